@@ -1,0 +1,222 @@
+"""Pins for the CPU oracle: closed forms, invariants, special cases and an
+independent brute force.  None of these re-types the oracle's own formulas."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import bruteforce, transformer as T
+from paper_2410_02425_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def tiny_shape(Hq=4, Hkv=2, d=16, F=24, V=32, L=2, dtype=synth.DTYPE_F32):
+    return synth.ModelShape("pin", L, d, Hq, Hkv, F, V, dtype=dtype)
+
+
+def cfg_of(shape):
+    return dict(n_layers=shape.n_layers, d_model=shape.d_model, n_heads=shape.n_heads,
+                n_kv_heads=shape.n_kv_heads, ffn_dim=shape.ffn_dim, vocab=shape.vocab,
+                rope_theta=shape.rope_theta, norm_eps=shape.norm_eps)
+
+
+def model(shape, seed=3, std=0.3, gain_std=0.2):
+    w = synth.model_weights(shape, seed, std=std, gain_std=gain_std)
+    return T.Model(cfg_of(shape), w), w
+
+
+# ------------------------------------------------------------------ RMSNorm
+
+def test_rmsnorm_mean_square_closed_form():
+    rng = np.random.default_rng(0)
+    x = rng.normal(size=(5, 64)) * 3.0
+    eps = 1e-5
+    y = T.rmsnorm(x, np.ones(64), eps)
+    ms = np.mean(x * x, axis=-1)
+    np.testing.assert_allclose(np.mean(y * y, axis=-1), ms / (ms + eps), rtol=1e-12)
+
+
+def test_rmsnorm_scale_invariant_and_gain():
+    rng = np.random.default_rng(1)
+    x = rng.normal(size=(3, 32))
+    g = rng.uniform(0.5, 2.0, size=32)
+    np.testing.assert_allclose(T.rmsnorm(7.5 * x, g, 0.0), T.rmsnorm(x, g, 0.0), rtol=1e-12)
+    # a constant row normalises to +-1 times the gain
+    c = np.full((1, 32), -4.0)
+    np.testing.assert_allclose(T.rmsnorm(c, g, 0.0)[0], -g, rtol=1e-12)
+
+
+# ------------------------------------------------------------------ softmax
+
+def test_softmax_rows_sum_to_one_and_shift_invariant():
+    rng = np.random.default_rng(2)
+    s = rng.normal(size=(6, 50)) * 10
+    p = T.softmax(s)
+    np.testing.assert_allclose(p.sum(-1), 1.0, atol=1e-12)
+    np.testing.assert_allclose(T.softmax(s + 123.0), p, rtol=1e-12)
+    one_hot = T.softmax(np.array([[0.0, 800.0, 0.0]]))
+    np.testing.assert_array_equal(one_hot, [[0.0, 1.0, 0.0]])
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(3)
+    hd = 8
+    k = rng.normal(size=(5, 1, hd))
+    v = rng.normal(size=(5, 1, hd))
+    # single visible key -> its value
+    q = rng.normal(size=(1, 1, hd))
+    out = T.attention(q, k, v, [0], np.arange(5), 1)
+    np.testing.assert_allclose(out[0, 0], v[0, 0], rtol=1e-12)
+    # zero query -> uniform weights -> mean of visible values
+    out = T.attention(np.zeros((1, 1, hd)), k, v, [3], np.arange(5), 1)
+    np.testing.assert_allclose(out[0, 0], v[:4, 0].mean(0), rtol=1e-12)
+
+
+# ------------------------------------------------------------------ RoPE
+
+def test_rope_identity_at_zero_and_norm_preserving():
+    rng = np.random.default_rng(4)
+    x = rng.normal(size=(1, 3, 16))
+    np.testing.assert_allclose(T.rope(x, np.array([0]), 10000.0), x, rtol=0, atol=0)
+    y = T.rope(np.repeat(x, 4, 0), np.array([1, 17, 300, 4999]), 10000.0)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(np.repeat(x, 4, 0), axis=-1), rtol=1e-12)
+
+
+def test_rope_scores_depend_only_on_relative_position():
+    rng = np.random.default_rng(5)
+    q = rng.normal(size=(1, 1, 32))
+    k = rng.normal(size=(1, 1, 32))
+    def dot(m, n):
+        return float(np.sum(T.rope(q, np.array([m]), 500.0) * T.rope(k, np.array([n]), 500.0)))
+    ref = dot(7, 3)
+    for m, n in [(4, 0), (104, 100), (4003, 3999)]:
+        assert abs(dot(m, n) - ref) < 1e-9
+    assert abs(dot(8, 3) - ref) > 1e-3
+
+
+def test_rope_matches_complex_rotation():
+    rng = np.random.default_rng(6)
+    x = rng.normal(size=(1, 1, 8))
+    got = T.rope(x, np.array([11]), 10000.0)[0, 0]
+    z = x[0, 0, :4] + 1j * x[0, 0, 4:]
+    z = z * np.exp(1j * 11 * 10000.0 ** (-np.arange(4) / 4.0))
+    np.testing.assert_allclose(got, np.concatenate([z.real, z.imag]), rtol=1e-12)
+
+
+# ------------------------------------------------------------------ SwiGLU, greedy
+
+def test_silu_closed_form():
+    from scipy.special import expit
+    z = np.linspace(-30, 30, 1001)
+    np.testing.assert_allclose(T.silu(z), z * expit(z), rtol=1e-12, atol=1e-300)
+    assert T.silu(np.array([0.0]))[0] == 0.0
+
+
+def test_greedy_ties_lowest_index():
+    assert T.greedy(np.array([1.0, 3.0, 2.0, 3.0])) == 1
+    assert bruteforce.greedy([1.0, 3.0, 2.0, 3.0]) == 1
+
+
+# ------------------------------------------------------------------ GQA
+
+def test_gqa_equals_mha_with_duplicated_kv_heads():
+    gqa_shape = tiny_shape(Hq=4, Hkv=2)
+    m_gqa, w = model(gqa_shape)
+    mha_shape = tiny_shape(Hq=4, Hkv=4)
+    w2 = dict(w)
+    hd = gqa_shape.head_dim
+    for layer in range(gqa_shape.n_layers):
+        for nm in ("wk", "wv"):
+            a = w[f"layers.{layer}.{nm}"].reshape(2, hd, -1)
+            w2[f"layers.{layer}.{nm}"] = np.repeat(a, 2, axis=0).reshape(4 * hd, -1)
+    m_mha = T.Model(cfg_of(mha_shape), w2)
+    toks = [3, 9, 1, 30, 7]
+    np.testing.assert_allclose(T.forward(m_gqa, toks, T.KVCache(m_gqa), "all"),
+                               T.forward(m_mha, toks, T.KVCache(m_mha), "all"), rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------------ whole model vs brute force
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 2), (2, 2)])
+def test_forward_matches_bruteforce(Hq, Hkv):
+    shape = tiny_shape(Hq=Hq, Hkv=Hkv)
+    m, w = model(shape)
+    toks = [5, 0, 31, 17, 17, 2, 9]
+    got = T.forward(m, toks, T.KVCache(m), "all")
+    ref = np.array(bruteforce.logits_all_positions(
+        dict(cfg_of(shape)), {k: np.asarray(v, np.float64) for k, v in w.items()}, toks))
+    np.testing.assert_allclose(got, ref, rtol=1e-9, atol=1e-9)
+
+
+def test_causal_mask_future_token_does_not_change_past():
+    m, _ = model(tiny_shape())
+    a = T.forward(m, [1, 2, 3, 4, 5, 6], T.KVCache(m), "all")
+    b = T.forward(m, [1, 2, 3, 4, 29, 6], T.KVCache(m), "all")
+    np.testing.assert_array_equal(a[:4], b[:4])
+    assert np.max(np.abs(a[4:] - b[4:])) > 1e-6
+
+
+def test_kv_cached_decode_equals_recompute():
+    m, _ = model(tiny_shape(), std=0.5)
+    prompt = [4, 8, 15, 16, 23, 1]
+    t1, l1 = T.generate(m, prompt, 9)
+    t2, l2 = T.generate_recompute(m, prompt, 9)
+    np.testing.assert_array_equal(t1, t2)
+    np.testing.assert_allclose(l1, l2, rtol=1e-10, atol=1e-10)
+
+
+def test_generate_first_token_from_prompt_pass_and_forcing():
+    m, _ = model(tiny_shape(), std=0.5)
+    prompt = [3, 1, 4, 1, 5]
+    toks, logits = T.generate(m, prompt, 4)
+    full = T.forward(m, prompt + list(toks[:3]), T.KVCache(m), "all")
+    np.testing.assert_allclose(logits, full[len(prompt) - 1:], rtol=1e-10, atol=1e-10)
+    forced = [7, 7, 7]
+    _, lf = T.generate(m, prompt, 4, forced=forced)
+    full = T.forward(m, prompt + forced, T.KVCache(m), "all")
+    np.testing.assert_allclose(lf, full[len(prompt) - 1:], rtol=1e-10, atol=1e-10)
+
+
+def test_batch_of_requests_is_independent():
+    m, _ = model(tiny_shape(), std=0.5)
+    prompts = [[1, 2, 3], [9, 9], [30, 1, 4, 1]]
+    caches = [T.KVCache(m) for _ in prompts]
+    for p, c in zip(prompts, caches):
+        T.forward(m, p, c)
+    batch = T.decode_step_batch(m, caches, [5, 6, 7])
+    caches2 = [T.KVCache(m) for _ in prompts]
+    for p, c in zip(prompts, caches2):
+        T.forward(m, p, c)
+    alone = T.decode_step_batch(m, caches2[1:2], [6])
+    np.testing.assert_array_equal(batch[1], alone[0])
+
+
+# ------------------------------------------------------------------ input generator
+
+def test_philox_known_answers():
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.txt")) as f:
+        rows = [l.split() for l in f if l.strip() and not l.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        v = [int(x, 16) for x in r]
+        out = synth.philox4x32_10(*v[:4], v[4], v[5])
+        assert [int(o) for o in out] == v[6:]
+
+
+def test_weight_generator_moments_and_random_access():
+    idx = np.arange(200000)
+    v = synth.normal_f32(99, 4, idx, 0.02)
+    assert abs(v.mean()) < 3e-4 and abs(v.std() - 0.02) < 2e-4
+    sub = synth.normal_f32(99, 4, idx[12345:12350], 0.02)
+    np.testing.assert_array_equal(sub, v[12345:12350])
+    assert not np.array_equal(synth.normal_f32(99, 5, idx[:100], 0.02), v[:100])
+
+
+def test_bf16_rounding_nearest_even():
+    x = np.array([1.0, 1.00390625, 1.01171875, -2.5e-3, 3.0e38], dtype=np.float32)
+    b = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(x))
+    # 1 + 2^-8 is a tie -> even (1.0); 1 + 3*2^-8 is a tie -> even (1 + 2^-6)
+    assert b[0] == 1.0 and b[1] == 1.0 and b[2] == np.float32(1.015625)
+    assert abs(b[3] - x[3]) <= abs(x[3]) * 2 ** -8
