@@ -1,0 +1,196 @@
+/* lp.h -- C ABI of the MI355X batched LLM serving step.
+ *
+ * The library runs the computation an LLM inference server performs while it
+ * is being benchmarked (LLM-Pilot, Sec. II-A/B and III-C): requests with
+ * varying numbers of input and output tokens are admitted into one running
+ * batch under continuous batching and a maximum batch weight (Sec. II-B);
+ * each request's prompt is processed in a prefill step that fills its KV cache
+ * and yields its first output token (Sec. II-A); decode steps then extend the
+ * KV cache and yield one token per active request each (Sec. II-A).  Per
+ * request the library reports every output token, the time to first token
+ * (TTFT, including queueing) and the inter-token latencies (ITL) of the
+ * following tokens (Sec. III-C-3).
+ *
+ * Conventions
+ *  - Every function returns an int status: LP_OK (0) or a negative LP_E* code;
+ *    lp_last_error() then holds a message.  No C++ exception crosses the ABI.
+ *  - The caller owns every host buffer passed in; the library copies what it
+ *    keeps.  Output buffers are caller-allocated with the documented sizes.
+ *  - Device memory: the caller provides one device buffer (the arena) and a
+ *    HIP stream at creation; the arena must outlive the engine.  The engine
+ *    places weights, KV cache and workspace inside the arena and allocates no
+ *    bulk device memory of its own.
+ *  - Times are int64 nanoseconds on one timeline whose origin is the start of
+ *    lp_run(); open-loop arrival times are given on that timeline.
+ *  - An engine is not thread-safe; distinct engines are independent.
+ */
+#ifndef LP_H
+#define LP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LP_OK 0
+#define LP_EINVAL (-1)  /* bad argument: config, lengths, token ids, sizes   */
+#define LP_ENOMEM (-2)  /* arena too small for weights + KV cache + workspace */
+#define LP_EHIP (-3)    /* a HIP runtime error                                */
+#define LP_ESTATE (-4)  /* call out of order (e.g. run before weights)        */
+
+#define LP_F32 0        /* fp32 weights and activations                        */
+#define LP_BF16 1       /* bf16 weights, bf16 GEMM inputs, fp32 accumulation   */
+
+#define LP_OPEN_LOOP 0   /* requests arrive at their given arrival_ns          */
+#define LP_CLOSED_LOOP 1 /* `concurrency` users with zero think time           */
+
+/* engine option flags */
+#define LP_FLAG_KEEP_LOGITS 1u  /* keep fp32 logits of every output token      */
+#define LP_FLAG_TIME_KERNEL 2u  /* time each decode gate/up GEMM launch        */
+
+/* Decoder shape.  Llama-style pre-norm decoder: RMSNorm, rotary embeddings
+ * (rotate-half pairing), grouped-query attention, SwiGLU MLP, untied LM head,
+ * no biases.  head_dim = d_model / n_heads. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, ffn_dim, vocab;
+  float rope_theta; /* RoPE base, e.g. 10000                                  */
+  float norm_eps;   /* RMSNorm epsilon, e.g. 1e-5                              */
+  int32_t dtype;    /* LP_F32 or LP_BF16                                       */
+} lp_model_config;
+
+typedef struct {
+  int32_t max_batch;          /* running-batch rows (KV slots), 1..64         */
+  int32_t max_seq_len;        /* largest in_len + out_len of one request      */
+  int64_t max_batch_weight;   /* Sec. II-B budget in tokens; 0 = all the KV
+                                 cache the arena holds                        */
+  int64_t max_prefill_tokens; /* prompt tokens in one prefill step            */
+  int64_t hbm_reserve_bytes;  /* arena bytes to leave unused                  */
+  uint32_t flags;             /* LP_FLAG_*                                    */
+} lp_engine_options;
+
+typedef struct {
+  int64_t id;            /* caller's id, unique within one submission          */
+  const int32_t *prompt; /* in_len token ids in [0, vocab)                     */
+  int32_t in_len;        /* >= 1                                               */
+  int32_t out_len;       /* >= 1; exactly this many tokens are generated       */
+  int64_t arrival_ns;    /* open loop: arrival time; closed loop: ignored      */
+} lp_request;
+
+typedef struct {
+  int32_t kind;     /* 0 = prefill, 1 = decode                                 */
+  int32_t n_rows;   /* requests in the step                                    */
+  int64_t n_tokens; /* prompt tokens (prefill) or rows (decode)                */
+  int64_t sum_ctx;  /* KV entries attended over, summed over rows              */
+  int64_t plan_ns;  /* when the host planned the iteration holding the step    */
+  int64_t end_ns;   /* when the step's last kernel finished                    */
+} lp_step_record;
+
+typedef struct {
+  int64_t n_steps, n_prefill_steps, n_decode_steps;
+  int64_t output_tokens, prompt_tokens;
+  int64_t wall_ns;               /* first arrival to last token                */
+  int64_t decode_ns;             /* summed decode step durations               */
+  int64_t decode_tokens;         /* tokens produced by decode steps            */
+  int64_t full_decode_steps;     /* decode steps with max_batch rows           */
+  int64_t full_decode_ns;        /* their summed durations                     */
+  int64_t full_decode_sum_ctx;   /* their summed KV context                    */
+  int64_t timed_kernel_launches; /* LP_FLAG_TIME_KERNEL: launches timed        */
+  double timed_kernel_ms;        /* ... and their summed durations             */
+} lp_run_stats;
+
+typedef struct lp_engine lp_engine;
+
+/* Bytes of arena an engine with this config and options needs: weights, the
+ * KV cache for max_batch_weight tokens (or max_batch * max_seq_len when it is
+ * 0) and workspace.  The caller allocates at least this many bytes. */
+int lp_arena_bytes_required(const lp_model_config *cfg, const lp_engine_options *opt,
+                            size_t *out_bytes);
+
+/* Creates an engine inside `arena` (device memory, 256-byte aligned,
+ * `arena_bytes` long) working on `hip_stream` (a hipStream_t, may be NULL for
+ * the null stream).  LP_ENOMEM if the arena cannot hold the weights, the
+ * workspace and a KV cache of max_batch_weight tokens (the paper's OOM while
+ * probing the maximum batch weight, Sec. III-C-2). */
+int lp_engine_create(const lp_model_config *cfg, const lp_engine_options *opt, void *arena,
+                     size_t arena_bytes, void *hip_stream, lp_engine **out);
+
+/* Loads all weights from a host blob: tensors in canonical order -- embedding
+ * [vocab x d]; per layer: attn_norm [d], wq [Hq*hd x d], wk [Hkv*hd x d],
+ * wv [Hkv*hd x d], wo [d x Hq*hd], mlp_norm [d], w_gate [F x d], w_up [F x d],
+ * w_down [d x F]; final_norm [d]; lm_head [vocab x d] -- each row-major
+ * [out x in], elements in the model dtype (fp32, or bf16 bit patterns).
+ * `bytes` must equal the exact blob size.  Synchronous. */
+int lp_load_weights(lp_engine *e, const void *host_blob, size_t bytes);
+
+/* Fills all weights on the device from the counter-based generator
+ * (Philox4x32-10 keyed by `seed`, counter = (element index, tensor id); the
+ * sum of twelve 10-bit uniforms gives an approximately normal value scaled to
+ * `std`); gains are set to 1.  Element (r, c) of canonical tensor t gets the
+ * same value as the host generator.  Synchronous. */
+int lp_init_weights_random(lp_engine *e, uint64_t seed, float std);
+
+/* The maximum batch weight in effect (tokens). */
+int lp_query_max_batch_weight(lp_engine *e, int64_t *out_tokens);
+
+/* Replaces the request set with `n` requests (prompts are copied to the
+ * device now, so lp_run starts with its inputs resident).  LP_EINVAL when a
+ * request can never be admitted: in_len < 1, out_len < 1, in_len + out_len >
+ * max_seq_len or > max_batch_weight, in_len > max_prefill_tokens, a token id
+ * outside [0, vocab), or duplicate ids. */
+int lp_submit(lp_engine *e, const lp_request *reqs, int32_t n);
+
+/* Teacher forcing (parity checks only): the k-th decode step of request `id`
+ * feeds toks[k] instead of the token it produced (n <= out_len - 1).  Call
+ * after lp_submit. */
+int lp_set_forced_tokens(lp_engine *e, int64_t id, const int32_t *toks, int32_t n);
+
+/* Serves every submitted request to completion.  mode LP_CLOSED_LOOP: the
+ * first `concurrency` requests arrive at time 0 and each finished request
+ * releases the next one at its finish time; LP_OPEN_LOOP: arrivals as given.
+ * May be called again to serve the same requests anew. */
+int lp_run(lp_engine *e, int32_t mode, int32_t concurrency);
+
+/* Per-request results of the last run.  tokens: out_len int32; itl_ns:
+ * out_len - 1 int64 (may be NULL); ttft_ns, e2e_ns, arrival_ns: scalars (may
+ * be NULL).  e2e == ttft + sum(itl) exactly. */
+int lp_get_result(lp_engine *e, int64_t id, int32_t *tokens, int64_t *ttft_ns, int64_t *itl_ns,
+                  int64_t *e2e_ns, int64_t *arrival_ns);
+
+/* Token times (out_len int64) of one request in the last run. */
+int lp_get_token_times(lp_engine *e, int64_t id, int64_t *token_ns);
+
+int lp_get_run_stats(lp_engine *e, lp_run_stats *out);
+
+/* Copies up to `cap` step records of the last run; *n_out = number of steps.
+ * If ids/slots are non-NULL they receive, step after step, the request id
+ * and slot of every row (caller sizes them from the sum of n_rows). */
+int lp_get_step_log(lp_engine *e, lp_step_record *out, int64_t cap, int64_t *n_out,
+                    int64_t *ids, int32_t *slots, int64_t ids_cap);
+
+/* fp32 logits [vocab] that produced output token k (0-based) of request id in
+ * the last run.  Needs LP_FLAG_KEEP_LOGITS. */
+int lp_get_logits(lp_engine *e, int64_t id, int32_t k, float *logits);
+
+const char *lp_last_error(const lp_engine *e);
+void lp_engine_destroy(lp_engine *e);
+
+/* Runs the same admission policy and accounting on the host with a synthetic
+ * step-time model instead of the GPU: duration = a_prefill + b_prefill *
+ * prompt tokens for a prefill step, a_decode + b_decode * rows for a decode
+ * step (ns).  Outputs as lp_get_step_log / lp_get_token_times: step records
+ * (cap `step_cap`), the id and slot of every row (cap `row_cap`), and every
+ * request's token times packed in submission order (cap `tok_cap`), arrival
+ * times (n).  For testing the scheduler without a GPU. */
+int lp_sched_simulate(const lp_request *reqs, int32_t n, int32_t max_batch,
+                      int64_t max_batch_weight, int64_t max_prefill_tokens, int32_t mode,
+                      int32_t concurrency, int64_t a_prefill, int64_t b_prefill, int64_t a_decode,
+                      int64_t b_decode, lp_step_record *steps, int64_t step_cap, int64_t *n_steps,
+                      int64_t *row_ids, int32_t *row_slots, int64_t row_cap, int64_t *token_ns,
+                      int64_t tok_cap, int64_t *arrival_ns);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LP_H */

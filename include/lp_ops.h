@@ -1,0 +1,76 @@
+/* lp_ops.h -- single-kernel entry points of the serving step, for parity
+ * checks and kernel timing.  They launch exactly the kernels the engine runs,
+ * on caller-provided device buffers, asynchronously on `hip_stream` (a
+ * hipStream_t, NULL for the null stream).  All pointers are device pointers
+ * unless stated otherwise; the caller owns every buffer.  Each returns LP_OK or
+ * LP_EINVAL (bad sizes; checked before any launch) or LP_EHIP (launch error);
+ * lp_last_error(NULL) then holds a message.
+ *
+ * `dtype` is LP_F32 or LP_BF16: the element type of weights and activations
+ * (bf16 as raw 16-bit patterns).  Accumulation is fp32 in both.
+ */
+#ifndef LP_OPS_H
+#define LP_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "lp.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Y[M x N] (fp32, row stride N) = X[M x K] (row stride ldx) times W[N x K]^T:
+ * the weight-GEMM contraction of every projection of the decoder (Q/K/V,
+ * output, gate/up, down, LM head).  bf16 with M <= 64 takes the decode
+ * kernel; `k_splits` > 1 splits K across workgroups and needs `ws` of at
+ * least k_splits * M * N * 4 bytes (fp32 partials).  Larger M takes the
+ * prefill kernel.  K must be a multiple of 8, N even; 16-byte aligned rows. */
+int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
+               int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* RMSNorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g for r < rows; x fp32
+ * [rows x d] (first incremented in place by the n_part fp32 partial arrays
+ * part[s][rows][d] when n_part > 0), g fp32 [d], y [rows x d] in dtype.
+ * d <= 8192. */
+int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t n_part, const float *g, void *y,
+                  int32_t rows, int32_t d, float eps, void *hip_stream);
+
+/* Decode attention of one layer (Sec. II-A's decode phase reads the KV cache
+ * of every earlier position).  q, out: [M x Hq x hd] in dtype.  KV cache of
+ * one layer in blocks of 64 tokens: k_cache [n_blocks][Hkv][64][hd],
+ * v_cache [n_blocks][Hkv][hd][64] (transposed per block); block_table
+ * [*][max_blocks] int32 lists each slot's blocks.  Row m reads slot
+ * row_slot[m] over positions 0..row_pos[m] (ctx = row_pos[m] + 1 <= max_ctx).
+ * ws: at least lp_op_decode_attention_ws_bytes(M, Hq, hd, max_ctx) bytes. */
+size_t lp_op_decode_attention_ws_bytes(int32_t M, int32_t n_heads, int32_t head_dim, int32_t max_ctx);
+int lp_op_decode_attention(int32_t dtype, const void *q, void *out, const void *k_cache, const void *v_cache,
+                           const int32_t *block_table, int32_t max_blocks, int64_t n_blocks,
+                           const int32_t *row_slot, const int32_t *row_pos, int32_t M, int32_t n_heads,
+                           int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, void *ws, size_t ws_bytes,
+                           void *hip_stream);
+
+/* Causal prefill attention of one layer over packed prompts (Sec. II-A's
+ * prompt processing): sequence j owns rows [seq_start[j], seq_start[j+1]) of
+ * q/out ([rows x Hq x hd]) at positions 0.., and its keys/values are already
+ * in the cache of slot seq_slot[j] (layout as above).  max_len bounds every
+ * sequence length. */
+int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, const void *k_cache, const void *v_cache,
+                            const int32_t *block_table, int32_t max_blocks, int64_t n_blocks,
+                            const int32_t *seq_start, const int32_t *seq_slot, int32_t n_seq, int32_t max_len,
+                            int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, void *hip_stream);
+
+/* Greedy decoding: tokens[m] = argmax of logits row m (fp32, row stride ld),
+ * lowest index on ties. */
+int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t *tokens, void *hip_stream);
+
+/* The device weight generator (see lp_init_weights_random): dst[rows x cols]
+ * in dtype gets element (r, c) of canonical tensor `tensor_id`, unpermuted. */
+int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_t tensor_id, int64_t rows, int64_t cols,
+                      float std, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LP_OPS_H */

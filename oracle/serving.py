@@ -45,7 +45,7 @@ class Step:
     ids: list            # request ids, in row order
     slots: list          # slot of each row
     ctx: list            # tokens in the KV cache after the step, per row
-    plan_ns: int = 0
+    plan_ns: int = 0     # when the iteration holding this step was planned
     end_ns: int = 0
 
 
@@ -115,6 +115,7 @@ def simulate(requests, max_batch: int, max_batch_weight: int, max_prefill_tokens
             weight += r.in_len + r.out_len
         it += 1
         retired = []
+        plan_t = now
 
         def run_step(kind, rows, n_tokens):
             nonlocal now, step_idx
@@ -123,7 +124,7 @@ def simulate(requests, max_batch: int, max_batch_weight: int, max_prefill_tokens
                 end = int(step_ns[step_idx])
             else:
                 end = now + int(step_ns(kind, len(rows), n_tokens, sum_ctx))
-            st = Step(kind, [r.id for r, _ in rows], [], [c for _, c in rows], plan_ns=now, end_ns=end)
+            st = Step(kind, [r.id for r, _ in rows], [], [c for _, c in rows], plan_ns=plan_t, end_ns=end)
             step_idx += 1
             now = end
             return st

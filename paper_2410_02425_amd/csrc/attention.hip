@@ -1,0 +1,290 @@
+// Attention over the paged KV cache.
+//
+// Decode: each request row attends to its whole cached context.  The context
+// is cut into chunks of DEC_CHUNK positions; one workgroup handles one (row,
+// kv head, chunk) and all query heads of that kv head's group, four waves each
+// taking one 64-position KV block.  Partial (max, sum, unnormalised output)
+// triples are merged by a combine pass (log-sum-exp rescaling).
+//
+// Prefill: causal attention of packed prompt rows, one workgroup per 64 query
+// rows of one (sequence, head), online softmax over 64-key blocks.
+#include "device.hpp"
+
+namespace lp {
+
+constexpr int DEC_CHUNK = 256;  // positions per decode workgroup
+constexpr int MAX_GROUP = 8;    // query heads per kv head
+
+size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx) {
+  const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
+  return (size_t)M * n_heads * splits * (head_dim + 2) * sizeof(float);
+}
+
+template <typename T>
+struct Vec8;  // 8 consecutive activation elements as fp32
+template <>
+struct Vec8<bf16_t> {
+  static __device__ __forceinline__ void load(const bf16_t *p, float *o) {
+    const uint4 u = *(const uint4 *)p;
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = __uint_as_float(w[i] << 16);
+      o[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+};
+template <>
+struct Vec8<float> {
+  static __device__ __forceinline__ void load(const float *p, float *o) {
+    const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+};
+
+template <typename T, int HD, int G>
+__global__ __launch_bounds__(256) void decode_attn_kernel(const T *__restrict__ q, RowMeta rows,
+                                                          KVCache kv, int layer, int n_heads,
+                                                          int max_splits, float *__restrict__ ws) {
+  constexpr int DPL = HD / 64;  // dims per lane in P.V
+  __shared__ float qs[G][HD];
+  __shared__ float ps[4][G][64];
+  __shared__ float wm[4][G], wl[4][G];
+  __shared__ float wo[4][G][HD];
+  const int s = blockIdx.x, g = blockIdx.y, m = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int slot = rows.row_slot[m];
+  const int ctx = rows.row_pos[m] + 1;
+  if (s * DEC_CHUNK >= ctx) return;
+
+  for (int e = threadIdx.x; e < G * HD; e += 256)
+    qs[e / HD][e % HD] = Act<T>::ld(q[((int64_t)m * n_heads + g * G) * HD + e]);
+  __syncthreads();
+
+  const int blk_pos = s * DEC_CHUNK + wave * 64;  // first position of this wave's block
+  const bool active = blk_pos < ctx;
+  float mw[G], lw[G], o[G][DPL];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    mw[h] = -INFINITY;
+    lw[h] = 0.f;
+#pragma unroll
+    for (int t = 0; t < DPL; ++t) o[h][t] = 0.f;
+  }
+  if (active) {
+    const int64_t base = kv_block_base(kv, layer, slot, blk_pos, g);
+    const T *kb = (const T *)kv.k + base;
+    const T *vb = (const T *)kv.v + base;
+    const int p = blk_pos + lane;
+    const bool valid = p < ctx;
+    float sc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) sc[h] = 0.f;
+    if (valid) {
+#pragma unroll 4
+      for (int d = 0; d < HD; d += 8) {
+        float kk[8];
+        Vec8<T>::load(kb + (int64_t)lane * HD + d, kk);
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+          for (int t = 0; t < 8; ++t) sc[h] += qs[h][d + t] * kk[t];
+      }
+    }
+    const float scale = rsqrtf((float)HD);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float sv = valid ? sc[h] * scale : -INFINITY;
+      mw[h] = wave_max(sv);
+      const float pv = valid ? __expf(sv - mw[h]) : 0.f;
+      lw[h] = wave_sum(pv);
+      ps[wave][h][lane] = pv;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    const int nvalid = min(64, ctx - blk_pos);
+#pragma unroll
+    for (int t = 0; t < DPL; ++t) {
+      const int d = lane * DPL + t;
+      const T *vr = vb + (int64_t)d * KV_BLOCK;
+      for (int pp = 0; pp < nvalid; pp += 8) {
+        float vv[8];
+        Vec8<T>::load(vr + pp, vv);
+        // cache entries past the context are stale or uninitialised: never read them as numbers
+#pragma unroll
+        for (int u = 0; u < 8; ++u) vv[u] = (pp + u < nvalid) ? vv[u] : 0.f;
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) o[h][t] += ps[wave][h][pp + u] * vv[u];
+      }
+    }
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      wm[wave][h] = mw[h];
+      wl[wave][h] = lw[h];
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int t = 0; t < DPL; ++t) wo[wave][h][lane * DPL + t] = o[h][t];
+  __syncthreads();
+
+  // merge the four waves and write this split's partial
+  for (int e = threadIdx.x; e < G * (HD + 2); e += 256) {
+    const int h = e / (HD + 2), c = e % (HD + 2);
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, wm[w][h]);
+    float acc = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (wm[w][h] == -INFINITY) continue;
+      const float f = __expf(wm[w][h] - M);
+      acc += f * (c < HD ? wo[w][h][c] : wl[w][h]);
+    }
+    float *dst = ws + (((int64_t)m * n_heads + g * G + h) * max_splits + s) * (HD + 2);
+    dst[c] = (c == HD) ? M : acc;  // [0, HD): output, HD: max, HD + 1: sum
+  }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_heads, int max_splits,
+                                                            const float *__restrict__ ws,
+                                                            T *__restrict__ out) {
+  const int h = blockIdx.x, m = blockIdx.y;
+  const int c = threadIdx.x;
+  const int ctx = rows.row_pos[m] + 1;
+  const int ns = (ctx + DEC_CHUNK - 1) / DEC_CHUNK;
+  const float *src = ws + ((int64_t)m * n_heads + h) * max_splits * (HD + 2);
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, src[s * (HD + 2) + HD]);
+  float num = 0.f, den = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float f = __expf(src[s * (HD + 2) + HD] - M);
+    num += f * src[s * (HD + 2) + c];
+    den += f * src[s * (HD + 2) + HD + 1];
+  }
+  out[((int64_t)m * n_heads + h) * HD + c] = Act<T>::st(num / den);
+}
+
+template <typename T, int HD>
+static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
+                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
+  const int G = n_heads / kv.n_kv_heads;
+  const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
+  dim3 grid(splits, kv.n_kv_heads, M);
+  switch (G) {
+    case 1: decode_attn_kernel<T, HD, 1><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
+    case 2: decode_attn_kernel<T, HD, 2><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
+    case 4: decode_attn_kernel<T, HD, 4><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
+    case 8: decode_attn_kernel<T, HD, 8><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
+    default: return;
+  }
+  decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, splits, ws, out);
+}
+
+template <typename T>
+void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
+                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
+  if (M <= 0) return;
+  if (kv.head_dim == 128)
+    launch_decode_hd<T, 128>(q, out, rows, kv, layer, M, n_heads, max_ctx, ws, s);
+  else if (kv.head_dim == 64)
+    launch_decode_hd<T, 64>(q, out, rows, kv, layer, M, n_heads, max_ctx, ws, s);
+}
+
+// ------------------------------------------------------------------ prefill
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void prefill_attn_kernel(const T *__restrict__ q, T *__restrict__ out,
+                                                           const int32_t *seq_start,
+                                                           const int32_t *seq_slot, KVCache kv,
+                                                           int layer, int n_heads) {
+  constexpr int Q4 = HD / 4;  // dims per thread
+  __shared__ T ks[64][HD + 2];
+  __shared__ T vs[64][HD + 2];
+  const int qt = blockIdx.x, h = blockIdx.y, j = blockIdx.z;
+  const int row0 = seq_start[j];
+  const int len = seq_start[j + 1] - row0;
+  if (qt * 64 >= len) return;
+  const int slot = seq_slot[j];
+  const int g = h / (n_heads / kv.n_kv_heads);
+  const int qi = threadIdx.x >> 2, qq = threadIdx.x & 3;
+  const int qpos = qt * 64 + qi;
+  const bool qvalid = qpos < len;
+  float qv[Q4], o[Q4];
+  const T *qr = q + ((int64_t)(row0 + (qvalid ? qpos : 0)) * n_heads + h) * HD + qq * Q4;
+#pragma unroll
+  for (int t = 0; t < Q4; ++t) {
+    qv[t] = Act<T>::ld(qr[t]);
+    o[t] = 0.f;
+  }
+  float mx = -INFINITY, l = 0.f;
+  const float scale = rsqrtf((float)HD);
+  const int last_key = min(len, qt * 64 + 64);  // keys [0, last_key)
+  for (int kb = 0; kb * 64 < last_key; ++kb) {
+    __syncthreads();
+    const int64_t base = kv_block_base(kv, layer, slot, kb * 64, g);
+    const T *kbp = (const T *)kv.k + base;
+    const T *vbp = (const T *)kv.v + base;
+    for (int e = threadIdx.x; e < 64 * HD; e += 256) {
+      const int p = e / HD, d = e % HD;
+      ks[p][d] = kbp[e];
+      const int d2 = e / 64, p2 = e % 64;
+      vs[p2][d2] = vbp[e];
+    }
+    __syncthreads();
+    const int nk = min(64, last_key - kb * 64);
+    for (int p = 0; p < nk; ++p) {
+      float sc = 0.f;
+#pragma unroll
+      for (int t = 0; t < Q4; ++t) sc += qv[t] * Act<T>::ld(ks[p][qq * Q4 + t]);
+      sc += __shfl_xor(sc, 1, 64);
+      sc += __shfl_xor(sc, 2, 64);
+      const int kpos = kb * 64 + p;
+      if (kpos > qpos) continue;  // causal (uniform across the 4 threads of a row)
+      sc *= scale;
+      const float mn = fmaxf(mx, sc);
+      const float corr = __expf(mx - mn);
+      const float pe = __expf(sc - mn);
+      l = l * corr + pe;
+#pragma unroll
+      for (int t = 0; t < Q4; ++t) o[t] = o[t] * corr + pe * Act<T>::ld(vs[p][qq * Q4 + t]);
+      mx = mn;
+    }
+  }
+  if (qvalid) {
+    T *orow = out + ((int64_t)(row0 + qpos) * n_heads + h) * HD + qq * Q4;
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int t = 0; t < Q4; ++t) orow[t] = Act<T>::st(o[t] * inv);
+  }
+}
+
+template <typename T>
+void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, const int32_t *seq_slot,
+                              int n_seq, int max_len, const KVCache &kv, int layer, int n_heads,
+                              hipStream_t s) {
+  if (n_seq <= 0) return;
+  dim3 grid((max_len + 63) / 64, n_heads, n_seq);
+  if (kv.head_dim == 128)
+    prefill_attn_kernel<T, 128><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+  else if (kv.head_dim == 64)
+    prefill_attn_kernel<T, 64><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+}
+
+#define INST(T)                                                                                     \
+  template void launch_decode_attention<T>(const T *, T *, const RowMeta &, const KVCache &, int,   \
+                                           int, int, int, float *, hipStream_t);                    \
+  template void launch_prefill_attention<T>(const T *, T *, const int32_t *, const int32_t *, int, \
+                                            int, const KVCache &, int, int, hipStream_t);
+INST(float)
+INST(bf16_t)
+#undef INST
+
+}  // namespace lp

@@ -1,0 +1,118 @@
+// Device-side helpers shared by the kernel sources.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace lp {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round to nearest even (finite inputs).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+template <typename T>
+struct Act;
+template <>
+struct Act<float> {
+  static __device__ __forceinline__ float ld(float v) { return v; }
+  static __device__ __forceinline__ float st(float v) { return v; }
+};
+template <>
+struct Act<bf16_t> {
+  static __device__ __forceinline__ float ld(bf16_t v) { return bf16_to_f32(v); }
+  static __device__ __forceinline__ bf16_t st(float v) { return f32_to_bf16(v); }
+};
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+// Element offset of (layer, slot-position, kv head) in the K cache (row of hd)
+// and the V cache (column inside a transposed [hd][BS] block).
+__device__ __forceinline__ int64_t kv_block_base(const KVCache &kv, int layer, int slot, int pos,
+                                                 int h) {
+  const int blk = kv.block_table[(int64_t)slot * kv.max_blocks + pos / KV_BLOCK];
+  return (((int64_t)layer * kv.n_blocks + blk) * kv.n_kv_heads + h) * (int64_t)KV_BLOCK * kv.head_dim;
+}
+
+// Applies the epilogue to output columns (n, n+1) of row m, n even.
+template <typename T>
+__device__ __forceinline__ void epi_pair(const Epi &ep, int m, int n, float v0, float v1) {
+  switch (ep.kind) {
+    case EPI_STORE:
+    case EPI_LOGITS: {
+      float2 *p = (float2 *)(ep.out + (int64_t)m * ep.ldo + n);
+      *p = make_float2(v0, v1);
+      break;
+    }
+    case EPI_RESID: {
+      float2 *p = (float2 *)(ep.out + (int64_t)m * ep.ldo + n);
+      float2 r = *p;
+      r.x += v0;
+      r.y += v1;
+      *p = r;
+      break;
+    }
+    case EPI_SILU: {
+      T *h = (T *)ep.act_out;
+      h[(int64_t)m * ep.ld_act + (n >> 1)] = Act<T>::st(silu(v0) * v1);
+      break;
+    }
+    case EPI_QKV: {
+      const int hd = ep.kv.head_dim;
+      const int qdim = ep.n_heads * hd;
+      const int kvdim = ep.kv.n_kv_heads * hd;
+      const int slot = ep.rows.row_slot[m];
+      const int pos = ep.rows.row_pos[m];
+      if (n < qdim + kvdim) {
+        const bool is_q = n < qdim;
+        const int c = is_q ? n : n - qdim;
+        const int h = c / hd;
+        const int i = (c % hd) >> 1;  // rotary pair index
+        const float cs = ep.rope_cos[(int64_t)pos * (hd >> 1) + i];
+        const float sn = ep.rope_sin[(int64_t)pos * (hd >> 1) + i];
+        const float r0 = v0 * cs - v1 * sn;
+        const float r1 = v1 * cs + v0 * sn;
+        if (is_q) {
+          T *q = (T *)ep.act_out + (int64_t)m * ep.ld_act + h * hd;
+          q[i] = Act<T>::st(r0);
+          q[i + (hd >> 1)] = Act<T>::st(r1);
+        } else {
+          T *k = (T *)ep.kv.k + kv_block_base(ep.kv, ep.layer, slot, pos, h) +
+                 (int64_t)(pos % KV_BLOCK) * hd;
+          k[i] = Act<T>::st(r0);
+          k[i + (hd >> 1)] = Act<T>::st(r1);
+        }
+      } else {
+        const int c = n - qdim - kvdim;
+        const int h = c / hd;
+        const int j = c % hd;
+        T *vt = (T *)ep.kv.v + kv_block_base(ep.kv, ep.layer, slot, pos, h) + (pos % KV_BLOCK);
+        vt[(int64_t)j * KV_BLOCK] = Act<T>::st(v0);
+        vt[(int64_t)(j + 1) * KV_BLOCK] = Act<T>::st(v1);
+      }
+      break;
+    }
+  }
+}
+
+}  // namespace lp

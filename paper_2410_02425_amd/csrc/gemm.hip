@@ -1,0 +1,320 @@
+// Weight GEMMs Y = X W^T (X: [M x K] activations, W: [N x K] weights, both
+// K-contiguous) with fused epilogues.
+//
+//  * gemm_skinny: bf16 MFMA for decode-sized M <= 64.  The weight matrix is the
+//    large operand and is streamed once from HBM with 16-byte loads straight
+//    into MFMA operand registers; four waves split the K range of a workgroup
+//    and are reduced through LDS; optional split-K across workgroups writes
+//    fp32 partials reduced by a finishing pass.
+//  * gemm_big: bf16 MFMA for prefill-sized M, 128x128x64 tiles staged in LDS.
+//  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
+#include "device.hpp"
+
+namespace lp {
+
+__device__ __forceinline__ bf16x8_t load_bf16x8(const bf16_t *p) {
+  uint4 u = *(const uint4 *)p;
+  return __builtin_bit_cast(bf16x8_t, u);
+}
+__device__ __forceinline__ bf16x8_t zero_bf16x8() { return __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0)); }
+
+// ------------------------------------------------------------------ skinny (decode)
+
+template <int MT, int NSUB, int U>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restrict__ X, int64_t ldx,
+                                                          const bf16_t *__restrict__ W, int M, int N,
+                                                          int K, int kchunk, float *__restrict__ part,
+                                                          Epi ep) {
+  constexpr int TILES = MT * NSUB;
+  __shared__ floatx4_t red[4][TILES][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  const int n0 = blockIdx.x * NSUB * 16;
+  const int s = blockIdx.y;
+  const int kbeg = s * kchunk;
+  const int kend = min(K, kbeg + kchunk);
+  const int kw = (((kend - kbeg + 3) / 4) + 31) & ~31;
+  const int kw0 = kbeg + wave * kw;
+  const int kw1 = min(kend, kw0 + kw);
+
+  floatx4_t acc[MT][NSUB];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const bf16_t *wrow[NSUB];
+  bool nvalid[NSUB];
+#pragma unroll
+  for (int j = 0; j < NSUB; ++j) {
+    const int n = n0 + j * 16 + r16;
+    nvalid[j] = n < N;
+    wrow[j] = W + (int64_t)(nvalid[j] ? n : 0) * K;
+  }
+  const bf16_t *xrow[MT];
+  bool mvalid[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int m = i * 16 + r16;
+    mvalid[i] = m < M;
+    xrow[i] = X + (int64_t)(mvalid[i] ? m : 0) * ldx;
+  }
+
+  for (int k = kw0; k < kw1; k += 32 * U) {
+    bf16x8_t a[U][MT], b[U][NSUB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kk = k + u * 32 + kq;
+      const bool kv = kk < kw1;
+#pragma unroll
+      for (int j = 0; j < NSUB; ++j) b[u][j] = (kv && nvalid[j]) ? load_bf16x8(wrow[j] + kk) : zero_bf16x8();
+#pragma unroll
+      for (int i = 0; i < MT; ++i) a[u][i] = (kv && mvalid[i]) ? load_bf16x8(xrow[i] + kk) : zero_bf16x8();
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], b[u][j], acc[i][j], 0, 0, 0);
+  }
+
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j) red[wave][i * NSUB + j][lane] = acc[i][j];
+  __syncthreads();
+
+  // wave w finishes tiles w, w+4, ...: fixed summation order over waves.
+  for (int t = wave; t < TILES; t += 4) {
+    floatx4_t v = red[0][t][lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) v += red[w][t][lane];
+    const int i = t / NSUB, j = t % NSUB;
+    const int n = n0 + j * 16 + r16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = i * 16 + (lane >> 4) * 4 + r;
+      const float other = __shfl_xor(v[r], 1, 64);
+      if (gridDim.y > 1) {
+        if (m < M && n < N) part[((int64_t)s * M + m) * N + n] = v[r];
+      } else if ((lane & 1) == 0 && m < M && n < N) {
+        epi_pair<bf16_t>(ep, m, n, v[r], other);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ split-K finish
+
+template <typename T>
+__global__ void gemm_finish_kernel(const float *__restrict__ part, int splits, int M, int N, Epi ep) {
+  const int64_t half = (int64_t)N / 2;
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= (int64_t)M * half) return;
+  const int m = (int)(p / half);
+  const int n = (int)(p % half) * 2;
+  float v0 = 0.f, v1 = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    const float2 q = *(const float2 *)(part + ((int64_t)s * M + m) * N + n);
+    v0 += q.x;
+    v1 += q.y;
+  }
+  epi_pair<T>(ep, m, n, v0, v1);
+}
+
+template <typename T>
+void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s) {
+  const int64_t pairs = (int64_t)M * (N / 2);
+  if (pairs <= 0) return;
+  gemm_finish_kernel<T><<<(unsigned)((pairs + 255) / 256), 256, 0, s>>>(part, splits, M, N, ep);
+}
+
+// ------------------------------------------------------------------ big (prefill)
+
+constexpr int BG_BM = 128, BG_BN = 128, BG_BK = 64, BG_LDS = BG_BK + 8;
+
+__global__ __launch_bounds__(256) void gemm_big_kernel(const bf16_t *__restrict__ X, int64_t ldx,
+                                                       const bf16_t *__restrict__ W, int M, int N,
+                                                       int K, Epi ep) {
+  __shared__ bf16_t As[BG_BM][BG_LDS];
+  __shared__ bf16_t Bs[BG_BN][BG_LDS];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * BG_BM, n0 = blockIdx.x * BG_BN;
+
+  // global -> register staging: each thread moves 4 chunks of 16 B for A and B
+  uint4 ra[4], rb[4];
+#define BG_GLOAD(k0)                                                                            \
+  _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                               \
+    const int idx = tid + c * 256;                                                              \
+    const int row = idx >> 3, kk = (k0) + (idx & 7) * 8;                                        \
+    const int m = m0 + row, n = n0 + row;                                                       \
+    ra[c] = (m < M && kk < K) ? *(const uint4 *)(X + (int64_t)m * ldx + kk) : make_uint4(0, 0, 0, 0); \
+    rb[c] = (n < N && kk < K) ? *(const uint4 *)(W + (int64_t)n * K + kk) : make_uint4(0, 0, 0, 0);   \
+  }
+  floatx16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  BG_GLOAD(0)
+  for (int k0 = 0; k0 < K; k0 += BG_BK) {
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int row = idx >> 3, kc = (idx & 7) * 8;
+      *(uint4 *)&As[row][kc] = ra[c];
+      *(uint4 *)&Bs[row][kc] = rb[c];
+    }
+    __syncthreads();
+    if (k0 + BG_BK < K) {
+      BG_GLOAD(k0 + BG_BK)
+    }
+#pragma unroll
+    for (int ks = 0; ks < BG_BK / 16; ++ks) {
+      bf16x8_t a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = __builtin_bit_cast(bf16x8_t,
+                                  *(const uint4 *)&As[wm * 64 + i * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = __builtin_bit_cast(bf16x8_t,
+                                  *(const uint4 *)&Bs[wn * 64 + j * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // epilogue through LDS: each wave stages one 32x32 tile at a time, then its
+  // lanes apply the epilogue to column pairs
+  __syncthreads();
+  float *stage = (float *)&As[0][0] + wave * 32 * 33;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        stage[((r & 3) + 4 * (lane >> 5) + 8 * (r >> 2)) * 33 + (lane & 31)] = acc[i][j][r];
+      __syncthreads();
+      for (int p = lane; p < 32 * 16; p += 64) {
+        const int row = p >> 4, c = (p & 15) * 2;
+        const int m = m0 + wm * 64 + i * 32 + row;
+        const int n = n0 + wn * 64 + j * 32 + c;
+        if (m < M && n < N) epi_pair<bf16_t>(ep, m, n, stage[row * 33 + c], stage[row * 33 + c + 1]);
+      }
+      __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------------ fp32 path
+
+constexpr int F_BM = 64, F_BN = 64, F_BK = 16;
+
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__ X, int64_t ldx,
+                                                       const float *__restrict__ W, int M, int N, int K,
+                                                       Epi ep) {
+  __shared__ float Xs[F_BK][F_BM + 4];
+  __shared__ float Ws[F_BK][F_BN + 4];
+  const int tid = threadIdx.x;
+  const int ty = tid >> 4, tx = tid & 15;
+  const int m0 = blockIdx.y * F_BM, n0 = blockIdx.x * F_BN;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += F_BK) {
+    {
+      const int row = tid >> 2, kk = (tid & 3) * 4;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = k0 + kk + u;
+        const int m = m0 + row, n = n0 + row;
+        Xs[kk + u][row] = (m < M && k < K) ? X[(int64_t)m * ldx + k] : 0.f;
+        Ws[kk + u][row] = (n < N && k < K) ? W[(int64_t)n * K + k] : 0.f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < F_BK; ++k) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = Xs[k][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Ws[k][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; j += 2) {
+      const int n = n0 + tx * 4 + j;
+      if (n < N) epi_pair<float>(ep, m, n, acc[i][j], acc[i][j + 1]);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ dispatch
+
+template <int MT>
+static void launch_skinny_mt(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K,
+                             int splits, float *part, const Epi &ep, hipStream_t s) {
+  constexpr int NSUB = 4, U = 2;
+  int kchunk = (K + splits - 1) / splits;
+  kchunk = (kchunk + 31) & ~31;
+  splits = (K + kchunk - 1) / kchunk;
+  dim3 grid((N + NSUB * 16 - 1) / (NSUB * 16), splits);
+  gemm_skinny_kernel<MT, NSUB, U><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, kchunk, part, ep);
+}
+
+int skinny_effective_splits(int K, int splits) {
+  int kchunk = (K + splits - 1) / splits;
+  kchunk = (kchunk + 31) & ~31;
+  return (K + kchunk - 1) / kchunk;
+}
+
+template <>
+void launch_gemm<bf16_t>(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K, int splits,
+                         float *part, const Epi &ep, hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  if (M <= 64) {
+    if (splits < 1 || part == nullptr) splits = 1;
+    switch ((M + 15) / 16) {
+      case 1: launch_skinny_mt<1>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 2: launch_skinny_mt<2>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 3: launch_skinny_mt<3>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      default: launch_skinny_mt<4>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+    }
+    return;
+  }
+  dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);
+  gemm_big_kernel<<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+}
+
+template <>
+void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int N, int K, int splits,
+                        float *part, const Epi &ep, hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  dim3 grid((N + F_BN - 1) / F_BN, (M + F_BM - 1) / F_BM);
+  gemm_f32_kernel<<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+}
+
+template void launch_gemm_finish<float>(const float *, int, int, int, const Epi &, hipStream_t);
+template void launch_gemm_finish<bf16_t>(const float *, int, int, int, const Epi &, hipStream_t);
+
+}  // namespace lp

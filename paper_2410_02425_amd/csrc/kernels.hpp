@@ -1,0 +1,109 @@
+// Kernel launch interface shared by the engine and the op-level entry points.
+// All pointers are device pointers; every launch goes on the given stream.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lp {
+
+constexpr int KV_BLOCK = 64;  // tokens per KV-cache block
+
+// bf16 stored as raw 16-bit patterns.
+typedef uint16_t bf16_t;
+
+// Where the rows of a step read their token and write their results.
+struct RowMeta {
+  const int32_t *row_slot;  // [M] KV slot of each row
+  const int32_t *row_pos;   // [M] position of the row's token in its sequence
+};
+
+// KV cache of all layers: K [L][NB][Hkv][BS][hd], V transposed per block:
+// Vt [L][NB][Hkv][hd][BS]; element type = activation type.
+struct KVCache {
+  void *k;
+  void *v;
+  const int32_t *block_table;  // [max_batch][max_blocks]
+  int32_t max_blocks;          // blocks per slot
+  int64_t n_blocks;            // blocks per layer
+  int32_t n_kv_heads, head_dim;
+};
+
+enum EpiKind : int {
+  EPI_STORE = 0,   // out_f32[m, n] = acc
+  EPI_QKV = 1,     // RoPE on q/k pairs, q -> q_out, k/v -> KV cache
+  EPI_RESID = 2,   // resid[m, n] += acc
+  EPI_SILU = 3,    // h[m, n/2] = silu(acc[2f]) * acc[2f+1]
+  EPI_LOGITS = 4,  // logits[m, n] = acc (fp32)
+};
+
+// Arguments of the GEMM epilogues.  Columns are processed in pairs (n, n+1),
+// n even; the weight rows are stored so that each pair belongs together
+// (rotary pairs of q/k, gate/up rows of the MLP).
+struct Epi {
+  int kind;
+  float *out;        // EPI_STORE / EPI_LOGITS: [M x ldo] fp32; EPI_RESID: [M x ldo]
+  int64_t ldo;
+  void *act_out;     // EPI_QKV: q [M x Hq*hd]; EPI_SILU: h [M x F] (activation type)
+  int64_t ld_act;
+  // EPI_QKV
+  RowMeta rows;
+  KVCache kv;
+  int32_t layer, n_heads;
+  const float *rope_cos;  // [max_pos][hd/2]
+  const float *rope_sin;
+};
+
+// ---------------------------------------------------------------- launches
+
+// x[M, d] (fp32) = embedding rows; token of row m: pool[tok_idx[m]] if
+// tok_idx[m] >= 0, else slot_tok[row_slot[m]].
+template <typename T>
+void launch_embed(const T *E, const int32_t *pool, const int32_t *tok_idx, const int32_t *row_slot,
+                  const int32_t *slot_tok, float *x, int M, int d, hipStream_t s);
+
+// Optionally folds split-K partials into the residual (x[r] += sum_s part[s][r]),
+// then y[j] = rmsnorm(x[src(j)]) * g where src(j) = rows ? rows[j] : j.
+template <typename T>
+void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride,
+                    const int32_t *rows, const float *g, T *y, int M, int d, float eps,
+                    hipStream_t s);
+
+// Generic GEMM Y = X W^T with epilogue.  T = float or bf16_t.
+// splits > 1 (bf16, M <= 64 only): writes partials [splits][M][N] into `part`
+// and a following launch_gemm_finish applies the epilogue.
+template <typename T>
+void launch_gemm(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits,
+                 float *part, const Epi &ep, hipStream_t s);
+
+template <typename T>
+void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s);
+
+// Decode attention: row m attends to ctx = row_pos[m] + 1 cached positions of
+// its slot.  q [M][Hq][hd], out [M][Hq][hd] (activation type).  Uses
+// workspace `ws` (see decode_attention_ws_bytes).
+size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx);
+template <typename T>
+void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
+                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s);
+
+// Prefill (causal) attention over packed sequences: sequence j covers rows
+// [seq_start[j], seq_start[j+1]) at positions 0.., KV slot seq_slot[j].
+template <typename T>
+void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, const int32_t *seq_slot,
+                              int n_seq, int max_len, const KVCache &kv, int layer, int n_heads,
+                              hipStream_t s);
+
+// Greedy token per row (lowest index on ties): tok -> slot_tok[out_slot[m]]
+// and tok_log[m].
+void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t *out_slot,
+                   int32_t *slot_tok, int32_t *tok_log, hipStream_t s);
+
+// Weight generator: writes rows x cols values of canonical tensor `tensor_id`
+// to dst with row r stored at dst_row(r) = r_off + perm(r) (see kernels), in T.
+enum RowPerm : int { PERM_NONE = 0, PERM_ROPE = 1, PERM_GATE = 2, PERM_UP = 3 };
+template <typename T>
+void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
+                        int64_t cols, float stdv, int perm, int head_dim, hipStream_t s);
+void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s);
+
+}  // namespace lp

@@ -1,0 +1,211 @@
+// Embedding gather, RMSNorm (with split-K residual folding), greedy argmax and
+// the device-side weight generator.
+#include "device.hpp"
+
+namespace lp {
+
+// ------------------------------------------------------------------ embedding
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const T *__restrict__ E, const int32_t *pool,
+                                                    const int32_t *tok_idx, const int32_t *row_slot,
+                                                    const int32_t *slot_tok, float *__restrict__ x,
+                                                    int d) {
+  const int m = blockIdx.x;
+  const int ti = tok_idx[m];
+  const int tok = ti >= 0 ? pool[ti] : slot_tok[row_slot[m]];
+  const T *src = E + (int64_t)tok * d;
+  float *dst = x + (int64_t)m * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Act<T>::ld(src[c]);
+}
+
+template <typename T>
+void launch_embed(const T *E, const int32_t *pool, const int32_t *tok_idx, const int32_t *row_slot,
+                  const int32_t *slot_tok, float *x, int M, int d, hipStream_t s) {
+  if (M <= 0) return;
+  embed_kernel<T><<<M, 256, 0, s>>>(E, pool, tok_idx, row_slot, slot_tok, x, d);
+}
+
+// ------------------------------------------------------------------ RMSNorm
+
+constexpr int NORM_THREADS = 256;
+constexpr int NORM_MAX_PER_THREAD = 32;  // d <= 8192
+
+template <typename T>
+__global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(float *x, const float *part, int n_part,
+                                                               int64_t part_stride,
+                                                               const int32_t *rows,
+                                                               const float *__restrict__ g,
+                                                               T *__restrict__ y, int d, float eps) {
+  __shared__ float red[NORM_THREADS / 64];
+  const int j = blockIdx.x;
+  const int src = rows ? rows[j] : j;
+  float *xr = x + (int64_t)src * d;
+  float v[NORM_MAX_PER_THREAD];
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
+    const int c = threadIdx.x + e * NORM_THREADS;
+    if (c < d) {
+      float a = xr[c];
+      for (int s = 0; s < n_part; ++s) a += part[s * part_stride + (int64_t)src * d + c];
+      v[e] = a;
+      ss += a * a;
+    }
+  }
+  if (n_part) {
+#pragma unroll
+    for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
+      const int c = threadIdx.x + e * NORM_THREADS;
+      if (c < d) xr[c] = v[e];
+    }
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < NORM_THREADS / 64; ++w) tot += red[w];
+  const float r = rsqrtf(tot / (float)d + eps);
+  T *yr = y + (int64_t)j * d;
+#pragma unroll
+  for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
+    const int c = threadIdx.x + e * NORM_THREADS;
+    if (c < d) yr[c] = Act<T>::st(v[e] * r * g[c]);
+  }
+}
+
+template <typename T>
+void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride, const int32_t *rows,
+                    const float *g, T *y, int M, int d, float eps, hipStream_t s) {
+  if (M <= 0) return;
+  rmsnorm_kernel<T><<<M, NORM_THREADS, 0, s>>>(x, part, n_part, part_stride, rows, g, y, d, eps);
+}
+
+// ------------------------------------------------------------------ argmax
+
+__global__ __launch_bounds__(256) void argmax_kernel(const float *__restrict__ logits, int64_t ld, int V,
+                                                     const int32_t *out_slot, int32_t *slot_tok,
+                                                     int32_t *tok_log) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int m = blockIdx.x;
+  const float *row = logits + (int64_t)m * ld;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int c = threadIdx.x; c < V; c += 256) {
+    const float v = row[c];
+    if (v > best) {  // increasing c: the first maximum of this thread wins
+      best = v;
+      bi = c;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ov > best || (ov == best && oi < bi)) {
+      best = ov;
+      bi = oi;
+    }
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = best;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > best || (sv[w] == best && si[w] < bi)) {
+        best = sv[w];
+        bi = si[w];
+      }
+    if (out_slot) slot_tok[out_slot[m]] = bi;
+    tok_log[m] = bi;
+  }
+}
+
+void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t *out_slot,
+                   int32_t *slot_tok, int32_t *tok_log, hipStream_t s) {
+  if (M <= 0) return;
+  argmax_kernel<<<M, 256, 0, s>>>(logits, ld, V, out_slot, slot_tok, tok_log);
+}
+
+// ------------------------------------------------------------------ weight generator
+
+// Philox4x32 with ten rounds (Salmon et al., SC'11).
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c[0], hi0 = __umulhi(0xD2511F53u, c[0]);
+    const uint32_t lo1 = 0xCD9E8D57u * c[2], hi1 = __umulhi(0xCD9E8D57u, c[2]);
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+template <typename T>
+__global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t tid, int64_t rows,
+                                   int64_t cols, float stdv, int perm, int hd) {
+  const int64_t n = rows * cols;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t c[4] = {(uint32_t)e, (uint32_t)((uint64_t)e >> 32), tid, 0u};
+    philox4x32_10(c, k0, k1);
+    int s = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) s += (c[w] & 1023u) + ((c[w] >> 10) & 1023u) + ((c[w] >> 20) & 1023u);
+    const float v = ((float)(s - 6138) * stdv) * 0x1p-10f;
+    const int64_t r = e / cols, col = e % cols;
+    int64_t dr = r;
+    if (perm == PERM_ROPE) {
+      const int64_t h = r / hd, i = r % hd;
+      dr = h * hd + (i < hd / 2 ? 2 * i : 2 * (i - hd / 2) + 1);
+    } else if (perm == PERM_GATE) {
+      dr = 2 * r;
+    } else if (perm == PERM_UP) {
+      dr = 2 * r + 1;
+    }
+    dst[dr * cols + col] = Act<T>::st(v);
+  }
+}
+
+template <typename T>
+void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
+                        int64_t cols, float stdv, int perm, int head_dim, hipStream_t s) {
+  const int64_t n = rows * cols;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+  init_weight_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(dst, k0, k1, tensor_id, rows, cols, stdv,
+                                                        perm, head_dim);
+}
+
+__global__ void fill_f32_kernel(float *dst, int64_t n, float v) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x)
+    dst[e] = v;
+}
+
+void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s) {
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  if (n > 0) fill_f32_kernel<<<(unsigned)blocks, 256, 0, s>>>(dst, n, v);
+}
+
+#define INST(T)                                                                                   \
+  template void launch_embed<T>(const T *, const int32_t *, const int32_t *, const int32_t *,     \
+                                const int32_t *, float *, int, int, hipStream_t);                 \
+  template void launch_rmsnorm<T>(float *, const float *, int, int64_t, const int32_t *,          \
+                                  const float *, T *, int, int, float, hipStream_t);              \
+  template void launch_init_weight<T>(T *, uint32_t, uint32_t, uint32_t, int64_t, int64_t, float, \
+                                      int, int, hipStream_t);
+INST(float)
+INST(bf16_t)
+#undef INST
+
+}  // namespace lp

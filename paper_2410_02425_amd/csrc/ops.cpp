@@ -1,0 +1,147 @@
+// Single-kernel entry points (include/lp_ops.h).
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "../../include/lp_ops.h"
+#include "kernels.hpp"
+
+namespace lp {
+int skinny_effective_splits(int K, int splits);
+}
+using namespace lp;
+
+std::string &lp_global_error();
+#define lp_ops_err lp_global_error()
+
+#define OPCHK(cond, msg)          \
+  do {                            \
+    if (!(cond)) {                \
+      lp_ops_err = (msg);         \
+      return LP_EINVAL;           \
+    }                             \
+  } while (0)
+
+static int op_status() {
+  hipError_t s = hipGetLastError();
+  if (s != hipSuccess) {
+    lp_ops_err = hipGetErrorString(s);
+    return LP_EHIP;
+  }
+  return LP_OK;
+}
+
+extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
+                          int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *stream) {
+  OPCHK(X && W && Y && M >= 0 && N > 0 && K > 0, "gemm: bad pointers or sizes");
+  OPCHK(K % 8 == 0 && N % 2 == 0 && ldx >= K && ldx % 8 == 0, "gemm: K % 8, N % 2, ldx");
+  OPCHK(dtype == LP_F32 || dtype == LP_BF16, "gemm: dtype");
+  hipStream_t s = (hipStream_t)stream;
+  Epi ep{};
+  ep.kind = EPI_STORE;
+  ep.out = Y;
+  ep.ldo = N;
+  if (dtype == LP_BF16) {
+    int splits = 1;
+    if (M <= 64 && k_splits > 1) {
+      splits = skinny_effective_splits(K, k_splits);
+      OPCHK(ws && ws_bytes >= (size_t)splits * M * N * 4, "gemm: workspace too small for split-K");
+    }
+    launch_gemm<bf16_t>((const bf16_t *)X, ldx, (const bf16_t *)W, M, N, K, splits, (float *)ws, ep, s);
+    if (splits > 1) launch_gemm_finish<bf16_t>((const float *)ws, splits, M, N, ep, s);
+  } else {
+    launch_gemm<float>((const float *)X, ldx, (const float *)W, M, N, K, 1, nullptr, ep, s);
+  }
+  return op_status();
+}
+
+extern "C" int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t n_part, const float *g, void *y,
+                             int32_t rows, int32_t d, float eps, void *stream) {
+  OPCHK(x && g && y && rows >= 0 && d > 0 && d <= 8192 && n_part >= 0 && (n_part == 0 || part), "rmsnorm: args");
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LP_BF16)
+    launch_rmsnorm<bf16_t>(x, part, n_part, (int64_t)rows * d, nullptr, g, (bf16_t *)y, rows, d, eps, s);
+  else if (dtype == LP_F32)
+    launch_rmsnorm<float>(x, part, n_part, (int64_t)rows * d, nullptr, g, (float *)y, rows, d, eps, s);
+  else
+    OPCHK(false, "rmsnorm: dtype");
+  return op_status();
+}
+
+extern "C" size_t lp_op_decode_attention_ws_bytes(int32_t M, int32_t n_heads, int32_t head_dim, int32_t max_ctx) {
+  return decode_attention_ws_bytes(M, n_heads, head_dim, max_ctx);
+}
+
+static int check_heads(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int32_t dtype) {
+  OPCHK(n_heads > 0 && n_kv_heads > 0 && n_heads % n_kv_heads == 0, "attention: heads");
+  const int G = n_heads / n_kv_heads;
+  OPCHK(G == 1 || G == 2 || G == 4 || G == 8, "attention: group size must be 1, 2, 4 or 8");
+  OPCHK(head_dim == 64 || head_dim == 128, "attention: head_dim must be 64 or 128");
+  OPCHK(dtype == LP_BF16 || (dtype == LP_F32 && head_dim == 64), "attention: dtype / head_dim");
+  return LP_OK;
+}
+
+extern "C" int lp_op_decode_attention(int32_t dtype, const void *q, void *out, const void *k_cache,
+                                      const void *v_cache, const int32_t *block_table, int32_t max_blocks,
+                                      int64_t n_blocks, const int32_t *row_slot, const int32_t *row_pos, int32_t M,
+                                      int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx,
+                                      void *ws, size_t ws_bytes, void *stream) {
+  int rc = check_heads(n_heads, n_kv_heads, head_dim, dtype);
+  if (rc) return rc;
+  OPCHK(q && out && k_cache && v_cache && block_table && row_slot && row_pos && M >= 0 && max_ctx > 0,
+        "decode attention: args");
+  OPCHK(max_blocks * 64 >= max_ctx, "decode attention: max_blocks too small for max_ctx");
+  OPCHK(ws && ws_bytes >= decode_attention_ws_bytes(M, n_heads, head_dim, max_ctx), "decode attention: ws");
+  KVCache kv{(void *)k_cache, (void *)v_cache, block_table, max_blocks, n_blocks, n_kv_heads, head_dim};
+  RowMeta rows{row_slot, row_pos};
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LP_BF16)
+    launch_decode_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, rows, kv, 0, M, n_heads, max_ctx,
+                                    (float *)ws, s);
+  else
+    launch_decode_attention<float>((const float *)q, (float *)out, rows, kv, 0, M, n_heads, max_ctx, (float *)ws,
+                                   s);
+  return op_status();
+}
+
+extern "C" int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, const void *k_cache,
+                                       const void *v_cache, const int32_t *block_table, int32_t max_blocks,
+                                       int64_t n_blocks, const int32_t *seq_start, const int32_t *seq_slot,
+                                       int32_t n_seq, int32_t max_len, int32_t n_heads, int32_t n_kv_heads,
+                                       int32_t head_dim, void *stream) {
+  int rc = check_heads(n_heads, n_kv_heads, head_dim, dtype);
+  if (rc) return rc;
+  OPCHK(q && out && k_cache && v_cache && block_table && seq_start && seq_slot && n_seq >= 0 && max_len > 0,
+        "prefill attention: args");
+  OPCHK(max_blocks * 64 >= max_len, "prefill attention: max_blocks too small for max_len");
+  KVCache kv{(void *)k_cache, (void *)v_cache, block_table, max_blocks, n_blocks, n_kv_heads, head_dim};
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LP_BF16)
+    launch_prefill_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, seq_start, seq_slot, n_seq, max_len, kv, 0,
+                                     n_heads, s);
+  else
+    launch_prefill_attention<float>((const float *)q, (float *)out, seq_start, seq_slot, n_seq, max_len, kv, 0,
+                                    n_heads, s);
+  return op_status();
+}
+
+extern "C" int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t *tokens, void *stream) {
+  OPCHK(logits && tokens && M >= 0 && V > 0 && ld >= V, "argmax: args");
+  launch_argmax(logits, ld, M, V, nullptr, nullptr, tokens, (hipStream_t)stream);
+  return op_status();
+}
+
+extern "C" int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_t tensor_id, int64_t rows,
+                                 int64_t cols, float stdv, void *stream) {
+  OPCHK(dst && rows > 0 && cols > 0 && tensor_id >= 0, "init_weight: args");
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LP_BF16)
+    launch_init_weight<bf16_t>((bf16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
+                               cols, stdv, PERM_NONE, 0, s);
+  else if (dtype == LP_F32)
+    launch_init_weight<float>((float *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows, cols,
+                              stdv, PERM_NONE, 0, s);
+  else
+    OPCHK(false, "init_weight: dtype");
+  return op_status();
+}

@@ -135,18 +135,25 @@ def philox4x32_10(c0, c1, c2, c3, k0: int, k1: int):
     Returns four uint32 arrays.
     """
     c = [np.asarray(x, dtype=np.uint64) & _MASK32 for x in (c0, c1, c2, c3)]
-    c = list(np.broadcast_arrays(*c))
+    c = [np.ascontiguousarray(x) for x in np.broadcast_arrays(*c)]
     k0 &= 0xFFFFFFFF
     k1 &= 0xFFFFFFFF
+    sh = np.uint64(32)
     for r in range(10):
         if r:
             k0 = (k0 + _PHILOX_W0) & 0xFFFFFFFF
             k1 = (k1 + _PHILOX_W1) & 0xFFFFFFFF
-        p0 = _PHILOX_M0 * c[0]
-        p1 = _PHILOX_M1 * c[2]
-        hi0, lo0 = p0 >> np.uint64(32), p0 & _MASK32
-        hi1, lo1 = p1 >> np.uint64(32), p1 & _MASK32
-        c = [hi1 ^ c[1] ^ np.uint64(k0), lo1, hi0 ^ c[3] ^ np.uint64(k1), lo0]
+        p0 = c[0] * _PHILOX_M0
+        p1 = c[2] * _PHILOX_M1
+        n0 = p1 >> sh
+        n0 ^= c[1]
+        n0 ^= np.uint64(k0)
+        n2 = p0 >> sh
+        n2 ^= c[3]
+        n2 ^= np.uint64(k1)
+        p1 &= _MASK32
+        p0 &= _MASK32
+        c = [n0, p1, n2, p0]
     return [x.astype(np.uint32) for x in c]
 
 
@@ -156,17 +163,40 @@ def seed_key(seed: int):
     return seed & 0xFFFFFFFF, seed >> 32
 
 
-def normal_f32(seed: int, tensor_id: int, index, std: float) -> np.ndarray:
-    """Approximately N(0, std^2) fp32 values for element indices ``index``."""
-    idx = np.asarray(index, dtype=np.uint64)
-    k0, k1 = seed_key(seed)
-    w = philox4x32_10(idx & _MASK32, idx >> np.uint64(32), np.uint64(tensor_id), 0, k0, k1)
+_CHUNK = 1 << 16
+
+
+def _normal_chunk(idx: np.ndarray, tensor_id: int, k0: int, k1: int, std: float) -> np.ndarray:
+    c = philox4x32_10(idx & _MASK32, idx >> np.uint64(32), np.uint64(tensor_id), 0, k0, k1)
     s = np.zeros(idx.shape, dtype=np.int64)
-    for word in w:
+    for word in c:
         word = word.astype(np.int64)
         s += (word & 1023) + ((word >> 10) & 1023) + ((word >> 20) & 1023)
     k = (s - 6138).astype(np.float32)
     return (k * np.float32(std)) * np.float32(2.0 ** -10)
+
+
+def normal_f32(seed: int, tensor_id: int, index, std: float) -> np.ndarray:
+    """Approximately N(0, std^2) fp32 values for element indices ``index``.
+
+    Large requests are split into cache-sized chunks spread over threads (the
+    values do not depend on the split)."""
+    idx = np.asarray(index, dtype=np.uint64)
+    k0, k1 = seed_key(seed)
+    flat = idx.reshape(-1)
+    if flat.size <= _CHUNK:
+        return _normal_chunk(flat, tensor_id, k0, k1, std).reshape(idx.shape)
+    out = np.empty(flat.size, dtype=np.float32)
+    starts = range(0, flat.size, _CHUNK)
+
+    def work(a):
+        out[a:a + _CHUNK] = _normal_chunk(flat[a:a + _CHUNK], tensor_id, k0, k1, std)
+
+    import concurrent.futures as cf
+    import os
+    with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(work, starts))
+    return out.reshape(idx.shape)
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:

@@ -1,0 +1,100 @@
+"""Host-side checks of the C ABI: the library loads without a GPU, exports every
+function the headers declare, and its scheduler (driven by a synthetic
+step-time model) reproduces the oracle's schedule and accounting exactly."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import serving as S
+from paper_2410_02425_amd import lp, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in ("lp.h", "lp_ops.h"):
+        with open(os.path.join(ROOT, "include", h)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(lp_\w+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    L = lp.lib()
+    names = declared_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert names == set(lp.EXPORTED)
+
+
+def test_config_validation_without_gpu():
+    shape = synth.SHAPES["8b"]
+    cfg = lp.make_config(shape)
+    opt = lp.EngineOptions(64, 5120, 0, 65536, 0, 0)
+    n = lp.arena_bytes(cfg, opt)
+    # bf16 weights alone are 16.06 GB; KV for 64 x 5120 tokens is 42.9 GB
+    assert 16.0e9 + 42.9e9 < n < 16.0e9 + 42.9e9 + 8e9
+    bad = lp.make_config(shape)
+    bad.n_kv_heads = 7
+    with pytest.raises(lp.LPError):
+        lp.arena_bytes(bad, opt)
+    opt_bad = lp.EngineOptions(65, 5120, 0, 65536, 0, 0)
+    with pytest.raises(lp.LPError):
+        lp.arena_bytes(cfg, opt_bad)
+
+
+def _oracle_trace(reqs, mb, W, P, closed, U, ap, bp, ad, bd):
+    sreqs = [S.SimRequest(r.id, r.in_len, r.out_len, r.arrival_ns) for r in reqs]
+    step = lambda kind, n_rows, n_tokens, sum_ctx: ap + bp * n_tokens if kind == "prefill" else ad + bd * n_rows
+    return S.simulate(sreqs, mb, W, P, closed, U, step)
+
+
+@pytest.mark.parametrize("closed", [True, False])
+def test_engine_scheduler_matches_oracle(closed):
+    rng = np.random.default_rng(7 if closed else 8)
+    for trial in range(25):
+        n = int(rng.integers(1, 40))
+        reqs, t = [], 0
+        for i in range(n):
+            t += int(rng.integers(0, 3000))
+            reqs.append(synth.Request(1000 + i, rng.integers(0, 50, size=int(rng.integers(1, 60))).astype(np.int32),
+                                      int(rng.integers(1, 20)), t if not closed else 0))
+        mb = int(rng.integers(1, 9))
+        W = int(rng.integers(80, 400))
+        P = int(rng.integers(60, 300))
+        U = int(rng.integers(1, 12))
+        ap, bp, ad, bd = 500, int(rng.integers(1, 20)), 300, int(rng.integers(1, 30))
+        steps, toks, arr = lp.sched_simulate(reqs, mb, W, P, closed, U, ap, bp, ad, bd)
+        tr = _oracle_trace(reqs, mb, W, P, closed, U, ap, bp, ad, bd)
+        assert [(s["kind"], s["ids"], s["slots"], s["end_ns"]) for s in steps] == \
+               [(s.kind, s.ids, s.slots, s.end_ns) for s in tr.steps]
+        assert [s["plan_ns"] for s in steps] == [s.plan_ns for s in tr.steps]
+        assert toks == tr.token_ns
+        assert arr == tr.arrival_ns
+        for r in reqs:
+            ttft, itl, e2e = S.request_latencies(arr[r.id], toks[r.id])
+            assert e2e == ttft + sum(itl)
+
+
+def test_scheduler_rejects_unadmittable_request():
+    reqs = [synth.Request(0, np.zeros(50, np.int32), 60)]
+    with pytest.raises(lp.LPError):
+        lp.sched_simulate(reqs, 2, 100, 1000, True, 1, 1, 1, 1, 1)
+
+
+def test_scheduler_golden_schedule():
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "schedule_example.json")) as f:
+        g = json.load(f)
+    reqs = [synth.Request(i, np.zeros(a, np.int32), b) for i, a, b in g["requests"]]
+    for c in g["cases"]:
+        steps, toks, arr = lp.sched_simulate(reqs, g["max_batch"], c["max_batch_weight"], g["max_prefill_tokens"],
+                                             True, g["concurrency"], 10, 1, 5, 1)
+        assert [[s["kind"], s["ids"], s["slots"], s["end_ns"]] for s in steps] == c["steps"]
+        assert {str(k): v for k, v in toks.items()} == c["token_ns"]
+        assert {str(k): v for k, v in arr.items()} == c["arrival_ns"]

@@ -1,0 +1,227 @@
+"""Kernel-level parity on the GPU: every kernel of the serving step, called
+through the C ABI (include/lp_ops.h), against the float64 oracle on the same
+seeded inputs.  Sizes span several tiles plus ragged tails, and include the
+full 8B-shape decode shapes (checked on sampled outputs)."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import transformer as T
+from paper_2410_02425_amd import lp, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def bf16_values(rng, shape, scale=1.0):
+    """Random fp32 values that bf16 represents exactly."""
+    v = (rng.standard_normal(size=shape) * scale).astype(np.float32)
+    return synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(v)).reshape(shape)
+
+
+def to_dev(a, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(dtype).to(DEV)
+
+
+def gemm_bound(X, W, rows, cols):
+    """|error| bound for fp32 accumulation of sampled outputs: 1e-5 * sum|x||w|."""
+    return 1e-5 * np.abs(X[rows].astype(np.float64)) @ np.abs(W[cols].astype(np.float64)).T
+
+
+GEMM_CASES = [
+    # M, N, K, splits -- decode kernel (M <= 64) with and without split-K, tails in M, N and K
+    (1, 96, 256, 1), (16, 768, 256, 1), (37, 1376, 688, 3), (64, 1024, 256, 2),
+    (64, 6144, 4096, 6), (64, 4096, 14336, 8), (5, 2000, 1000, 4),
+    # prefill kernel
+    (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1),
+]
+
+
+@pytest.mark.parametrize("M,N,K,splits", GEMM_CASES)
+def test_gemm_bf16(M, N, K, splits):
+    rng = np.random.default_rng(M * 7 + N + K)
+    X = bf16_values(rng, (M, K))
+    W = bf16_values(rng, (N, K), 0.02)
+    Xd, Wd = to_dev(X, torch.bfloat16), to_dev(W, torch.bfloat16)
+    Y = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    ws = torch.empty(max(splits, 1) * M * N, dtype=torch.float32, device=DEV)
+    lp.op_gemm(Xd, Wd, Y, splits, ws)
+    torch.cuda.synchronize()
+    got = Y.cpu().numpy()
+    ref = X.astype(np.float64) @ W.astype(np.float64).T
+    bound = 1e-5 * (np.abs(X.astype(np.float64)) @ np.abs(W.astype(np.float64)).T) + 1e-12
+    assert np.all(np.abs(got - ref) <= bound), np.max(np.abs(got - ref) / bound)
+
+
+def test_gemm_bf16_full_8b_gate_up_sampled():
+    """The decode gate/up GEMM at its full 8B-shape size (M=64, N=2*14336,
+    K=4096), checked on 512 sampled outputs computed one by one."""
+    M, N, K = 64, 28672, 4096
+    g = torch.Generator().manual_seed(1234)
+    X = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    W = (torch.randn(N, K, generator=g) * 0.02).to(torch.bfloat16)
+    Y = torch.empty(M, N, dtype=torch.float32, device=DEV)
+    lp.op_gemm(X.to(DEV), W.to(DEV), Y, 1, None)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    rows, cols = rng.integers(0, M, 512), rng.integers(0, N, 512)
+    rows[:2], cols[:2] = [0, M - 1], [0, N - 1]
+    Xn, Wn = X.float().numpy().astype(np.float64), W.float().numpy().astype(np.float64)
+    got = Y.cpu().numpy()[rows, cols]
+    ref = np.einsum("ik,ik->i", Xn[rows], Wn[cols])
+    bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xn[rows]), np.abs(Wn[cols]))
+    assert np.all(np.abs(got - ref) <= bound)
+
+
+@pytest.mark.parametrize("M,N,K", [(3, 100, 64), (37, 1376, 688), (130, 768, 256)])
+def test_gemm_f32(M, N, K):
+    rng = np.random.default_rng(K)
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float32)
+    Y = torch.empty(M, N, dtype=torch.float32, device=DEV)
+    lp.op_gemm(to_dev(X, torch.float32), to_dev(W, torch.float32), Y)
+    torch.cuda.synchronize()
+    ref = X.astype(np.float64) @ W.astype(np.float64).T
+    bound = 1e-5 * (np.abs(X.astype(np.float64)) @ np.abs(W.astype(np.float64)).T) + 1e-12
+    assert np.all(np.abs(Y.cpu().numpy() - ref) <= bound)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,d,n_part", [(4, 256, 0), (64, 4096, 3), (7, 8192, 0), (33, 5120, 1)])
+def test_rmsnorm(dtype, rows, d, n_part):
+    rng = np.random.default_rng(rows + d)
+    x = (rng.standard_normal((rows, d)) * 3).astype(np.float32)
+    part = (rng.standard_normal((max(n_part, 1), rows, d))).astype(np.float32)
+    g = rng.uniform(0.5, 1.5, d).astype(np.float32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    xd = to_dev(x, torch.float32)
+    y = torch.empty(rows, d, dtype=tdt, device=DEV)
+    lp.op_rmsnorm(xd, to_dev(g, torch.float32), y, 1e-5, to_dev(part, torch.float32) if n_part else None, n_part)
+    torch.cuda.synchronize()
+    xs = x.astype(np.float64) + (part[:n_part].astype(np.float64).sum(0) if n_part else 0)
+    ref = T.rmsnorm(xs, g.astype(np.float64), 1e-5)
+    got = y.float().cpu().numpy()
+    tol = 1e-5 if dtype == "f32" else 2 ** -8
+    assert np.all(np.abs(got - ref) <= tol * np.abs(ref) + 1e-6)
+    if n_part:
+        np.testing.assert_allclose(xd.cpu().numpy(), xs, rtol=1e-6, atol=1e-5)
+
+
+def test_argmax_ties_and_tail():
+    rng = np.random.default_rng(3)
+    V = 128256
+    logits = rng.standard_normal((9, V)).astype(np.float32)
+    logits[0, [5, 77, 128255]] = 50.0      # tie: lowest index wins
+    logits[1, V - 1] = 60.0                # last element
+    logits[2, :] = 1.0                     # all equal -> 0
+    logits[3, 0] = 80.0
+    out = torch.empty(9, dtype=torch.int32, device=DEV)
+    lp.op_argmax(to_dev(logits, torch.float32), out)
+    torch.cuda.synchronize()
+    assert out.cpu().numpy().tolist() == [int(np.argmax(r)) for r in logits]
+    assert out.cpu().numpy()[:4].tolist() == [5, V - 1, 0, 0]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_device_weight_generator_matches_host(dtype):
+    rows, cols, tid, seed = 300, 688, 17, 0x1234ABCD5678
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    dst = torch.empty(rows, cols, dtype=tdt, device=DEV)
+    lp.op_init_weight(dst, seed, tid, 0.02)
+    torch.cuda.synchronize()
+    host = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02,
+                               synth.DTYPE_F32 if dtype == "f32" else synth.DTYPE_BF16)
+    got = dst.float().cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), host.view(np.uint32))
+
+
+# ------------------------------------------------------------------ attention
+
+def make_paged_cache(rng, ctx_lens, Hkv, hd, tdt, extra_blocks=3):
+    """Random KV cache in 64-token blocks with shuffled block tables.
+    Returns device (kc, vt, block_table) and the host per-slot K/V [ctx, Hkv, hd]."""
+    BS = 64
+    nb_slot = [(c + BS - 1) // BS for c in ctx_lens]
+    n_blocks = sum(nb_slot) + extra_blocks
+    perm = rng.permutation(n_blocks)
+    max_blocks = max(nb_slot)
+    bt = np.zeros((len(ctx_lens), max_blocks), dtype=np.int32)
+    kc = bf16_values(rng, (n_blocks, Hkv, BS, hd))
+    vt = bf16_values(rng, (n_blocks, Hkv, hd, BS))
+    used = 0
+    Ks, Vs = [], []
+    for s, c in enumerate(ctx_lens):
+        blocks = perm[used:used + nb_slot[s]]
+        used += nb_slot[s]
+        bt[s, :nb_slot[s]] = blocks
+        K = np.concatenate([kc[b] for b in blocks], axis=1)[:, :c]            # [Hkv, c, hd]
+        V = np.concatenate([vt[b] for b in blocks], axis=2)[:, :, :c]         # [Hkv, hd, c]
+        Ks.append(K.transpose(1, 0, 2))
+        Vs.append(V.transpose(2, 0, 1))
+    return (to_dev(kc, tdt), to_dev(vt, tdt), torch.from_numpy(bt).to(DEV)), Ks, Vs
+
+
+DECODE_CASES = [
+    # dtype, Hq, Hkv, hd, context lengths
+    ("bf16", 32, 8, 128, [1, 63, 64, 65, 256, 257, 700, 5120]),
+    ("bf16", 8, 8, 128, [300, 2, 1024]),
+    ("bf16", 64, 8, 128, [77, 4096]),
+    ("bf16", 4, 4, 64, [40, 33]),
+    ("f32", 4, 4, 64, [1, 40, 129, 600]),
+    ("f32", 8, 2, 64, [64, 65]),
+]
+
+
+@pytest.mark.parametrize("dtype,Hq,Hkv,hd,ctx", DECODE_CASES)
+def test_decode_attention(dtype, Hq, Hkv, hd, ctx):
+    rng = np.random.default_rng(len(ctx) * 100 + Hq)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    (kc, vt, bt), Ks, Vs = make_paged_cache(rng, ctx, Hkv, hd, tdt)
+    M = len(ctx)
+    q = bf16_values(rng, (M, Hq, hd))
+    out = torch.full((M, Hq, hd), float("nan"), dtype=tdt, device=DEV)
+    max_ctx = max(ctx)
+    ws = torch.empty(lp.decode_attention_ws_bytes(M, Hq, hd, max_ctx) // 4 + 1, dtype=torch.float32, device=DEV)
+    row_slot = torch.arange(M, dtype=torch.int32, device=DEV)
+    row_pos = torch.tensor([c - 1 for c in ctx], dtype=torch.int32, device=DEV)
+    lp.op_decode_attention(to_dev(q, tdt), out, kc, vt, bt, row_slot, row_pos, Hkv, max_ctx, ws)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    for m, c in enumerate(ctx):
+        ref = T.attention(q[m:m + 1].astype(np.float64), Ks[m].astype(np.float64), Vs[m].astype(np.float64),
+                          [c - 1], np.arange(c), Hkv)[0]
+        tol = 2e-5 if dtype == "f32" else 2 ** -8 * np.abs(ref) + 2e-3
+        assert np.all(np.abs(got[m] - ref) <= tol), (m, c, np.max(np.abs(got[m] - ref)))
+
+
+PREFILL_CASES = [
+    ("bf16", 32, 8, 128, [1, 17, 64, 65, 200]),
+    ("bf16", 8, 8, 128, [130, 3]),
+    ("bf16", 4, 4, 64, [32, 32, 32, 32]),
+    ("f32", 4, 4, 64, [32, 32, 5, 100]),
+    ("f32", 8, 2, 64, [70]),
+]
+
+
+@pytest.mark.parametrize("dtype,Hq,Hkv,hd,lens", PREFILL_CASES)
+def test_prefill_attention(dtype, Hq, Hkv, hd, lens):
+    rng = np.random.default_rng(sum(lens) + Hq)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    (kc, vt, bt), Ks, Vs = make_paged_cache(rng, lens, Hkv, hd, tdt)
+    rows = sum(lens)
+    q = bf16_values(rng, (rows, Hq, hd))
+    out = torch.full((rows, Hq, hd), float("nan"), dtype=tdt, device=DEV)
+    seq_start = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device=DEV)
+    seq_slot = torch.arange(len(lens), dtype=torch.int32, device=DEV)
+    lp.op_prefill_attention(to_dev(q, tdt), out, kc, vt, bt, seq_start, seq_slot, max(lens), Hkv)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    r0 = 0
+    for j, n in enumerate(lens):
+        ref = T.attention(q[r0:r0 + n].astype(np.float64), Ks[j].astype(np.float64), Vs[j].astype(np.float64),
+                          np.arange(n), np.arange(n), Hkv)
+        tol = 2e-5 if dtype == "f32" else 2 ** -8 * np.abs(ref) + 2e-3
+        assert np.all(np.abs(got[r0:r0 + n] - ref) <= tol), (j, np.max(np.abs(got[r0:r0 + n] - ref)))
+        r0 += n
