@@ -1,0 +1,219 @@
+"""Benchmark of the batched serving step on one MI355X.
+
+A step is one full serving run (every row of the hot path: admission and
+continuous batching under the batch-weight budget, packed prefill, KV-cached
+greedy decode, latency accounting) over the seeded 8B-shape GQA workload:
+256 requests, 64 concurrent users in a closed loop (the batch is held at 64 by
+continuous admission), input lengths lognormal(6.0, 0.8) clipped to [16, 4096],
+output lengths lognormal(5.0, 0.7) clipped to [8, 1024].  Weights are
+generated on the device (bf16 values ~N(0, 0.02)) and prompts are uploaded
+before the timed region.
+
+Prints one JSON line: whole-job output tokens/s over the timed steps, the
+decode throughput and HBM fraction of full-batch decode steps, p50 TTFT/ITL,
+the roofline of the dominant kernel (decode gate/up GEMM, timed per launch
+with HIP events inside the timed region) and the CPU oracle's rate on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2410_02425_amd import lp, synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def decode_step_bytes(shape: synth.ModelShape, rows: int, sum_ctx: int, esz: int = 2) -> int:
+    """Algorithmic HBM bytes of one decode step: every weight once (LM head
+    included), the KV cache of every row's context once, the new K/V entries,
+    and the embedding rows."""
+    d, hd, F, V, L = shape.d_model, shape.head_dim, shape.ffn_dim, shape.vocab, shape.n_layers
+    Hq, Hkv = shape.n_heads, shape.n_kv_heads
+    weights = esz * (L * (d * (Hq + 2 * Hkv) * hd + Hq * hd * d + 3 * d * F) + V * d)
+    gains = 4 * (L * 2 * d + d)
+    kv_read = sum_ctx * 2 * L * Hkv * hd * esz
+    kv_write = rows * 2 * L * Hkv * hd * esz
+    embed = rows * d * esz
+    return weights + gains + kv_read + kv_write + embed
+
+
+def gate_up_bytes(shape: synth.ModelShape, launches: int, rows_sum: int, esz: int = 2) -> int:
+    """Algorithmic bytes of the decode gate/up GEMM launches: the fused [2F x d]
+    weight once per launch, plus each launch's activation rows in and out."""
+    d, F = shape.d_model, shape.ffn_dim
+    return launches * 2 * F * d * esz + rows_sum * (d + F) * esz
+
+
+def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 25.0):
+    """The oracle, unchanged, on a bounded sample of the workload: one request
+    (prompt and output lengths taken from the workload) generated at depth 1
+    and 2 with full-width weights, extrapolated linearly in depth to the full
+    model.  Returns the oracle's tokens/s at full depth for that request."""
+    from oracle import transformer as T
+
+    r = sorted(reqs, key=lambda q: abs(q.in_len - 553))[0]
+    n_out = 6
+    times = {}
+    lm_rows = None
+    embed_rows = None
+    for depth in (1, 2):
+        sh = shape.with_layers(depth)
+        names = synth.tensor_shapes(sh)
+        w = {}
+        used = np.unique(r.prompt)
+        for name, tid, (rows, cols) in names:
+            if name == "embed":
+                if embed_rows is None:
+                    embed_rows = np.zeros((rows, cols), dtype=np.float32)
+                    embed_rows[used] = synth.tensor_values(seed, tid, used, cols, 0.02, sh.dtype)
+                w[name] = embed_rows
+            elif name == "lm_head":
+                if lm_rows is None:
+                    lm_rows = synth.tensor_values(seed, 2 + 9 * shape.n_layers, np.arange(rows), cols, 0.02,
+                                                  sh.dtype)
+                w[name] = lm_rows
+            else:
+                v = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02, sh.dtype, gain=synth.is_gain(name))
+                w[name] = v.reshape(cols) if rows == 1 else v
+        cfg = dict(n_layers=depth, d_model=sh.d_model, n_heads=sh.n_heads, n_kv_heads=sh.n_kv_heads,
+                   ffn_dim=sh.ffn_dim, vocab=sh.vocab, rope_theta=sh.rope_theta, norm_eps=sh.norm_eps)
+        m = T.Model(cfg, w)
+        t0 = time.perf_counter()
+        T.generate(m, r.prompt, n_out)
+        times[depth] = time.perf_counter() - t0
+        del m, w
+    per_layer = max(times[2] - times[1], 1e-9)
+    fixed = max(times[1] - per_layer, 0.0)
+    full = fixed + per_layer * shape.n_layers
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {
+        "value": n_out / full,
+        "unit": "output tokens/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"one 8B-shape request (in_len {r.in_len}, {n_out} output tokens), float64 oracle with "
+                   f"full-width weights at depth 1 ({times[1]:.1f} s) and 2 ({times[2]:.1f} s), extrapolated "
+                   f"linearly to {shape.n_layers} layers"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="8b")
+    ap.add_argument("--requests", type=int, default=0, help="override the workload's request count")
+    ap.add_argument("--act", choices=["f16", "bf16"], default="f16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    torch.cuda.set_device(0)
+    shape = synth.SHAPES[args.config]
+    wl = synth.WORKLOADS[args.config]
+    key = synth.workload_seeds(wl.base_seed)[0]
+    reqs = synth.make_requests(wl, shape.vocab, args.requests or None)
+    max_seq = wl.in_range[1] + wl.out_range[1]
+    flags = 0 if args.no_kernel_timing else lp.LP_FLAG_TIME_KERNEL
+    if args.act == "bf16":
+        flags |= lp.LP_FLAG_BF16_ACTIVATIONS
+    opt = lp.EngineOptions(wl.max_batch, max_seq, 0, 65536, 0, flags)
+    eng = lp.Engine(lp.make_config(shape), opt)
+    eng.init_weights_random(key, 0.02)
+    eng.submit(reqs)
+    mode = lp.LP_CLOSED_LOOP if wl.mode == "closed" else lp.LP_OPEN_LOOP
+    for _ in range(args.warmup):
+        eng.run(mode, wl.max_batch)
+        print(f"warmup run done: {eng.stats()['output_tokens']} tokens", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    agg = None
+    for k in range(args.steps):
+        eng.run(mode, wl.max_batch)
+        s = eng.stats()
+        agg = s if agg is None else {kk: agg[kk] + s[kk] for kk in s}
+        print(f"timed run {k + 1}/{args.steps}: {s['output_tokens']} tokens in {s['wall_ns'] / 1e9:.2f} s",
+              file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    # per-request latency medians (TTFT over requests, ITL pooled), last timed run
+    log = eng.step_log()
+    res = {r.id: eng.result(r.id) for r in reqs}
+    ttft = [res[r.id]["ttft_ns"] for r in reqs]
+    itl = np.concatenate([res[r.id]["itl_ns"] for r in reqs if r.out_len > 1])
+    nttft = [res[r.id]["ttft_ns"] / r.in_len for r in reqs]
+    # full-batch decode steps: throughput and HBM fraction
+    full = [st for st in log if st["kind"] == "decode" and st["n_rows"] == wl.max_batch]
+    prev_end = {i: (log[i - 1]["end_ns"] if i else 0) for i in range(len(log))}
+    full_idx = [i for i, st in enumerate(log) if st["kind"] == "decode" and st["n_rows"] == wl.max_batch]
+    full_ns = sum(log[i]["end_ns"] - prev_end[i] for i in full_idx)
+    full_bytes = sum(decode_step_bytes(shape, log[i]["n_rows"], log[i]["sum_ctx"]) for i in full_idx)
+    full_tokens = sum(log[i]["n_rows"] for i in full_idx)
+    decode_gbs = full_bytes / full_ns if full_ns else 0.0
+    out_tokens = agg["output_tokens"]
+
+    roofline = None
+    if agg["timed_kernel_launches"]:
+        launches = agg["timed_kernel_launches"]
+        avg_ms = agg["timed_kernel_ms"] / launches
+        bytes_total = gate_up_bytes(shape, launches, agg["timed_kernel_rows"])
+        achieved = bytes_total / launches / (avg_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "kernel": "gemm_skinny_kernel (decode gate/up, fused SiLU gate)",
+                    "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
+                    "bytes_per_launch": int(bytes_total / launches)}
+
+    result = {
+        "metric": "decode tokens/sec at fixed batch + p50 ITL/TTFT; % of HBM peak (1 MI355X)",
+        "value": round(out_tokens / elapsed, 1),
+        "unit": "output tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if args.act == "f16" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.config}-shape decoder, closed loop, {wl.max_batch} users, "
+                               f"{len(reqs)} requests, lognormal lengths",
+                   "weights": "bf16 values ~N(0,0.02), held exactly in fp16" if args.act == "f16"
+                   else "bf16 ~N(0,0.02)",
+                   "global_batch": wl.max_batch, "parallelism": "none (1 GPU)"},
+        "decode_tok_s_full_batch": round(full_tokens / (full_ns * 1e-9), 1) if full_ns else None,
+        "decode_hbm_gbs_full_batch": round(decode_gbs, 1),
+        "decode_hbm_frac_full_batch": round(decode_gbs / HBM_PEAK_GBS, 4),
+        "decode_ms_per_step_full_batch": round(full_ns / max(len(full_idx), 1) / 1e6, 3),
+        "ttft_p50_ms": round(float(np.median(ttft)) / 1e6, 2),
+        "nttft_p50_ms": round(float(np.median(nttft)) / 1e6, 4),
+        "itl_p50_ms": round(float(np.median(itl)) / 1e6, 3),
+        "prefill_steps": agg["n_prefill_steps"],
+        "decode_steps": agg["n_decode_steps"],
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(shape, reqs, key)
+    eng.close()
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

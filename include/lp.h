@@ -40,8 +40,13 @@ extern "C" {
 #define LP_EHIP (-3)    /* a HIP runtime error                                */
 #define LP_ESTATE (-4)  /* call out of order (e.g. run before weights)        */
 
-#define LP_F32 0        /* fp32 weights and activations                        */
-#define LP_BF16 1       /* bf16 weights, bf16 GEMM inputs, fp32 accumulation   */
+#define LP_F32 0  /* fp32 weights and activations                                */
+#define LP_BF16 1 /* bf16 weights; GEMM inputs and KV cache in fp16, which holds
+                     every bf16 value that is 0 or of magnitude in
+                     [2^-17, 65504] exactly (lp_load_weights rejects others),
+                     or with LP_FLAG_BF16_ACTIVATIONS in bf16; fp32
+                     accumulation                                               */
+#define LP_F16 2  /* element type of the single-kernel entry points: fp16      */
 
 #define LP_OPEN_LOOP 0   /* requests arrive at their given arrival_ns          */
 #define LP_CLOSED_LOOP 1 /* `concurrency` users with zero think time           */
@@ -49,6 +54,7 @@ extern "C" {
 /* engine option flags */
 #define LP_FLAG_KEEP_LOGITS 1u  /* keep fp32 logits of every output token      */
 #define LP_FLAG_TIME_KERNEL 2u  /* time each decode gate/up GEMM launch        */
+#define LP_FLAG_BF16_ACTIVATIONS 4u /* bf16 (not fp16) GEMM inputs and KV cache */
 
 /* Decoder shape.  Llama-style pre-norm decoder: RMSNorm, rotary embeddings
  * (rotate-half pairing), grouped-query attention, SwiGLU MLP, untied LM head,
@@ -97,6 +103,7 @@ typedef struct {
   int64_t full_decode_ns;        /* their summed durations                     */
   int64_t full_decode_sum_ctx;   /* their summed KV context                    */
   int64_t timed_kernel_launches; /* LP_FLAG_TIME_KERNEL: launches timed        */
+  int64_t timed_kernel_rows;     /* ... their summed activation rows (M)       */
   double timed_kernel_ms;        /* ... and their summed durations             */
 } lp_run_stats;
 

@@ -6,8 +6,8 @@
  * LP_EINVAL (bad sizes; checked before any launch) or LP_EHIP (launch error);
  * lp_last_error(NULL) then holds a message.
  *
- * `dtype` is LP_F32 or LP_BF16: the element type of weights and activations
- * (bf16 as raw 16-bit patterns).  Accumulation is fp32 in both.
+ * `dtype` is LP_F32, LP_BF16 or LP_F16: the element type of weights and
+ * activations (bf16 as raw 16-bit patterns).  Accumulation is fp32 in all.
  */
 #ifndef LP_OPS_H
 #define LP_OPS_H
@@ -66,7 +66,8 @@ int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, const void 
 int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t *tokens, void *hip_stream);
 
 /* The device weight generator (see lp_init_weights_random): dst[rows x cols]
- * in dtype gets element (r, c) of canonical tensor `tensor_id`, unpermuted. */
+ * in dtype gets element (r, c) of canonical tensor `tensor_id`, unpermuted;
+ * LP_F16 stores the bf16-rounded value (as a bf16 model held in fp16). */
 int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_t tensor_id, int64_t rows, int64_t cols,
                       float std, void *hip_stream);
 

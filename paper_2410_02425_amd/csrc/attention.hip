@@ -35,6 +35,14 @@ struct Vec8<bf16_t> {
   }
 };
 template <>
+struct Vec8<f16_t> {
+  static __device__ __forceinline__ void load(const f16_t *p, float *o) {
+    const f16x8_t v = __builtin_bit_cast(f16x8_t, *(const uint4 *)p);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (float)v[i];
+  }
+};
+template <>
 struct Vec8<float> {
   static __device__ __forceinline__ void load(const float *p, float *o) {
     const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
@@ -285,6 +293,7 @@ void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, cons
                                             int, const KVCache &, int, int, hipStream_t);
 INST(float)
 INST(bf16_t)
+INST(f16_t)
 #undef INST
 
 }  // namespace lp

@@ -8,6 +8,7 @@
 namespace lp {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef float floatx16_t __attribute__((ext_vector_type(16)));
 
@@ -32,6 +33,46 @@ struct Act<bf16_t> {
   static __device__ __forceinline__ float ld(bf16_t v) { return bf16_to_f32(v); }
   static __device__ __forceinline__ bf16_t st(float v) { return f32_to_bf16(v); }
 };
+
+template <>
+struct Act<f16_t> {
+  static __device__ __forceinline__ float ld(f16_t v) { return (float)v; }
+  static __device__ __forceinline__ f16_t st(float v) { return (f16_t)v; }
+};
+
+// MFMA instructions per 16-bit element type: 16x16x32 and 32x32x16 tiles,
+// fp32 accumulation.
+template <typename T>
+struct Mfma;
+template <>
+struct Mfma<bf16_t> {
+  typedef bf16x8_t v8;
+  static __device__ __forceinline__ floatx4_t m16(v8 a, v8 b, floatx4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ floatx16_t m32(v8 a, v8 b, floatx16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <>
+struct Mfma<f16_t> {
+  typedef f16x8_t v8;
+  static __device__ __forceinline__ floatx4_t m16(v8 a, v8 b, floatx4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ floatx16_t m32(v8 a, v8 b, floatx16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::v8 load8(const T *p) {
+  return __builtin_bit_cast(typename Mfma<T>::v8, *(const uint4 *)p);
+}
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::v8 zero8() {
+  return __builtin_bit_cast(typename Mfma<T>::v8, make_uint4(0, 0, 0, 0));
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

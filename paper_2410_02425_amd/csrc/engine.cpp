@@ -48,12 +48,16 @@ struct Layout {
   size_t total;
 };
 
+// Activation / weight storage type of the GPU path.
+enum ActType { ACT_F32 = 0, ACT_BF16 = 1, ACT_F16 = 2 };
+
 struct Dims {
   int L, d, Hq, Hkv, hd, F, V, qkv_n;
   size_t esz;  // bytes per activation / weight element
+  int act;     // ActType
 };
 
-Dims dims_of(const lp_model_config &c) {
+Dims dims_of(const lp_model_config &c, uint32_t flags = 0) {
   Dims D;
   D.L = c.n_layers;
   D.d = c.d_model;
@@ -64,6 +68,9 @@ Dims dims_of(const lp_model_config &c) {
   D.V = c.vocab;
   D.qkv_n = (D.Hq + 2 * D.Hkv) * D.hd;
   D.esz = c.dtype == LP_BF16 ? 2 : 4;
+  // a bf16 model computes with fp16 MFMA inputs by default: the bf16 weight
+  // values are held exactly and activations / KV entries round 8x finer
+  D.act = c.dtype == LP_F32 ? ACT_F32 : ((flags & LP_FLAG_BF16_ACTIVATIONS) ? ACT_BF16 : ACT_F16);
   return D;
 }
 
@@ -273,7 +280,7 @@ extern "C" int lp_engine_create(const lp_model_config *cfg, const lp_engine_opti
   lp_engine *e = new lp_engine();
   e->cfg = *cfg;
   e->opt = *opt;
-  e->D = dims_of(*cfg);
+  e->D = dims_of(*cfg, opt->flags);
   e->arena = (char *)arena;
   e->stream = (hipStream_t)hip_stream;
   e->max_blocks = (opt->max_seq_len + KV_BLOCK - 1) / KV_BLOCK;
@@ -424,6 +431,27 @@ extern "C" int lp_load_weights(lp_engine *e, const void *blob, size_t bytes) {
   }
   const char *src = (const char *)blob;
   std::vector<char> tmp;
+  std::vector<char> conv;
+  if (D.act == ACT_F16) {
+    // bf16 bit patterns -> fp16 bit patterns, exactly or not at all
+    const size_t n = bytes / 2;
+    conv.resize(bytes);
+    const uint16_t *b = (const uint16_t *)blob;
+    uint16_t *h = (uint16_t *)conv.data();
+    for (size_t i = 0; i < n; ++i) {
+      uint32_t u = (uint32_t)b[i] << 16;
+      float f;
+      memcpy(&f, &u, 4);
+      const _Float16 hv = (_Float16)f;
+      if ((float)hv != f) {
+        e->err = "a bf16 weight is not exactly representable in fp16; create the engine with "
+                 "LP_FLAG_BF16_ACTIVATIONS";
+        return LP_EINVAL;
+      }
+      memcpy(&h[i], &hv, 2);
+    }
+    src = conv.data();
+  }
   for (int i = 0; i < (int)ts.size(); ++i) {
     const auto &t = ts[i];
     const Dest ds = dest_of(e, i);
@@ -431,7 +459,11 @@ extern "C" int lp_load_weights(lp_engine *e, const void *blob, size_t bytes) {
     if (ds.gain) {
       std::vector<float> g(t.cols);
       for (int64_t c = 0; c < t.cols; ++c) {
-        if (D.esz == 2) {
+        if (D.act == ACT_F16) {
+          _Float16 hv;
+          memcpy(&hv, src + c * 2, 2);
+          g[c] = (float)hv;
+        } else if (D.esz == 2) {
           uint16_t b;
           memcpy(&b, src + c * 2, 2);
           uint32_t u = (uint32_t)b << 16;
@@ -470,12 +502,15 @@ extern "C" int lp_init_weights_random(lp_engine *e, uint64_t seed, float stdv) {
     const Dest ds = dest_of(e, i);
     if (ds.gain) {
       launch_fill_f32((float *)(e->arena + ds.off), t.cols, 1.0f, e->stream);
-    } else if (D.esz == 2) {
+    } else if (D.act == ACT_F16) {
+      launch_init_weight<f16_t>((f16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
+                                ds.perm, D.hd, true, e->stream);
+    } else if (D.act == ACT_BF16) {
       launch_init_weight<bf16_t>((bf16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                 ds.perm, D.hd, e->stream);
+                                 ds.perm, D.hd, false, e->stream);
     } else {
       launch_init_weight<float>((float *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                ds.perm, D.hd, e->stream);
+                                ds.perm, D.hd, false, e->stream);
     }
   }
   HIPCHK(e, hipGetLastError());
@@ -583,7 +618,7 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
   T *ab = e->ptr<T>(e->Ly.attn);
   T *hb = e->ptr<T>(e->Ly.h);
   float *part = e->ptr<float>(e->Ly.part);
-  const bool bf = D.esz == 2;
+  const bool bf = D.act != ACT_F32;
   const float eps = e->cfg.norm_eps;
   RowMeta rows{dm.row_slot, dm.row_pos};
   KVCache kv = kv_of<T>(e, dm.block_table);
@@ -723,15 +758,24 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int ring, int64_t log_o
   memcpy(h + o_bt, block_table_host.data(), block_table_host.size() * 4);
   HIPCHK(e, hipMemcpyAsync(d, h, o * 4, hipMemcpyHostToDevice, e->stream));
   StepMeta dm{d + o_slot, d + o_pos, d + o_tok, d + o_ss, d + o_sq, d + o_lm, d + o_bt};
-  const bool bf = e->D.esz == 2;
-  if (bf)
-    launch_embed<bf16_t>(e->ptr<bf16_t>(e->Ly.embed), e->ptr<int32_t>(e->Ly.pool), dm.row_tok, dm.row_slot,
-                         e->ptr<int32_t>(e->Ly.slot_tok), e->ptr<float>(e->Ly.x), M, e->D.d, e->stream);
-  else
-    launch_embed<float>(e->ptr<float>(e->Ly.embed), e->ptr<int32_t>(e->Ly.pool), dm.row_tok, dm.row_slot,
-                        e->ptr<int32_t>(e->Ly.slot_tok), e->ptr<float>(e->Ly.x), M, e->D.d, e->stream);
-  int rc = bf ? run_layers<bf16_t>(e, ps.kind == 0, M, n_rows, n_rows, max_len, dm, log_off, ring)
-              : run_layers<float>(e, ps.kind == 0, M, n_rows, n_rows, max_len, dm, log_off, ring);
+  int rc;
+  const bool pf = ps.kind == 0;
+  int32_t *pool = e->ptr<int32_t>(e->Ly.pool), *stok = e->ptr<int32_t>(e->Ly.slot_tok);
+  float *x = e->ptr<float>(e->Ly.x);
+  switch (e->D.act) {
+    case ACT_F16:
+      launch_embed<f16_t>(e->ptr<f16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
+      rc = run_layers<f16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+      break;
+    case ACT_BF16:
+      launch_embed<bf16_t>(e->ptr<bf16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d,
+                           e->stream);
+      rc = run_layers<bf16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+      break;
+    default:
+      launch_embed<float>(e->ptr<float>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
+      rc = run_layers<float>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+  }
   if (rc) return rc;
   HIPCHK(e, hipEventRecord(e->ev_step[ring], e->stream));
   return LP_OK;
@@ -761,6 +805,7 @@ int read_step(lp_engine *e, RunState &rs, int64_t k) {
       if (hipEventElapsedTime(&km, tk[0], tk[1]) == hipSuccess) {
         e->stats.timed_kernel_ms += km;
         e->stats.timed_kernel_launches += 1;
+        e->stats.timed_kernel_rows += e->steps[k].n_rows;
       }
     }
   }

@@ -12,17 +12,12 @@
 
 namespace lp {
 
-__device__ __forceinline__ bf16x8_t load_bf16x8(const bf16_t *p) {
-  uint4 u = *(const uint4 *)p;
-  return __builtin_bit_cast(bf16x8_t, u);
-}
-__device__ __forceinline__ bf16x8_t zero_bf16x8() { return __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0)); }
 
 // ------------------------------------------------------------------ skinny (decode)
 
-template <int MT, int NSUB, int U>
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restrict__ X, int64_t ldx,
-                                                          const bf16_t *__restrict__ W, int M, int N,
+template <typename T, int MT, int NSUB, int U>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const T *__restrict__ X, int64_t ldx,
+                                                          const T *__restrict__ W, int M, int N,
                                                           int K, int kchunk, float *__restrict__ part,
                                                           Epi ep) {
   constexpr int TILES = MT * NSUB;
@@ -43,7 +38,8 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restri
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  const bf16_t *wrow[NSUB];
+  typedef typename Mfma<T>::v8 v8;
+  const T *wrow[NSUB];
   bool nvalid[NSUB];
 #pragma unroll
   for (int j = 0; j < NSUB; ++j) {
@@ -51,7 +47,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restri
     nvalid[j] = n < N;
     wrow[j] = W + (int64_t)(nvalid[j] ? n : 0) * K;
   }
-  const bf16_t *xrow[MT];
+  const T *xrow[MT];
   bool mvalid[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
@@ -61,15 +57,15 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restri
   }
 
   for (int k = kw0; k < kw1; k += 32 * U) {
-    bf16x8_t a[U][MT], b[U][NSUB];
+    v8 a[U][MT], b[U][NSUB];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kk = k + u * 32 + kq;
       const bool kv = kk < kw1;
 #pragma unroll
-      for (int j = 0; j < NSUB; ++j) b[u][j] = (kv && nvalid[j]) ? load_bf16x8(wrow[j] + kk) : zero_bf16x8();
+      for (int j = 0; j < NSUB; ++j) b[u][j] = (kv && nvalid[j]) ? load8<T>(wrow[j] + kk) : zero8<T>();
 #pragma unroll
-      for (int i = 0; i < MT; ++i) a[u][i] = (kv && mvalid[i]) ? load_bf16x8(xrow[i] + kk) : zero_bf16x8();
+      for (int i = 0; i < MT; ++i) a[u][i] = (kv && mvalid[i]) ? load8<T>(xrow[i] + kk) : zero8<T>();
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -77,7 +73,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restri
       for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int j = 0; j < NSUB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], b[u][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = Mfma<T>::m16(a[u][i], b[u][j], acc[i][j]);
   }
 
 #pragma unroll
@@ -100,7 +96,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t *__restri
       if (gridDim.y > 1) {
         if (m < M && n < N) part[((int64_t)s * M + m) * N + n] = v[r];
       } else if ((lane & 1) == 0 && m < M && n < N) {
-        epi_pair<bf16_t>(ep, m, n, v[r], other);
+        epi_pair<T>(ep, m, n, v[r], other);
       }
     }
   }
@@ -135,11 +131,13 @@ void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &
 
 constexpr int BG_BM = 128, BG_BN = 128, BG_BK = 64, BG_LDS = BG_BK + 8;
 
-__global__ __launch_bounds__(256) void gemm_big_kernel(const bf16_t *__restrict__ X, int64_t ldx,
-                                                       const bf16_t *__restrict__ W, int M, int N,
+template <typename T>
+__global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, int64_t ldx,
+                                                       const T *__restrict__ W, int M, int N,
                                                        int K, Epi ep) {
-  __shared__ bf16_t As[BG_BM][BG_LDS];
-  __shared__ bf16_t Bs[BG_BN][BG_LDS];
+  typedef typename Mfma<T>::v8 v8;
+  __shared__ T As[BG_BM][BG_LDS];
+  __shared__ T Bs[BG_BN][BG_LDS];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
@@ -179,20 +177,16 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const bf16_t *__restrict_
     }
 #pragma unroll
     for (int ks = 0; ks < BG_BK / 16; ++ks) {
-      bf16x8_t a[2], b[2];
+      v8 a[2], b[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = __builtin_bit_cast(bf16x8_t,
-                                  *(const uint4 *)&As[wm * 64 + i * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
+      for (int i = 0; i < 2; ++i) a[i] = load8<T>(&As[wm * 64 + i * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = __builtin_bit_cast(bf16x8_t,
-                                  *(const uint4 *)&Bs[wn * 64 + j * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
+      for (int j = 0; j < 2; ++j) b[j] = load8<T>(&Bs[wn * 64 + j * 32 + (lane & 31)][ks * 16 + (lane >> 5) * 8]);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = Mfma<T>::m32(a[i], b[j], acc[i][j]);
     }
   }
 
@@ -212,7 +206,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const bf16_t *__restrict_
         const int row = p >> 4, c = (p & 15) * 2;
         const int m = m0 + wm * 64 + i * 32 + row;
         const int n = n0 + wn * 64 + j * 32 + c;
-        if (m < M && n < N) epi_pair<bf16_t>(ep, m, n, stage[row * 33 + c], stage[row * 33 + c + 1]);
+        if (m < M && n < N) epi_pair<T>(ep, m, n, stage[row * 33 + c], stage[row * 33 + c + 1]);
       }
       __syncthreads();
     }
@@ -271,15 +265,15 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 
 // ------------------------------------------------------------------ dispatch
 
-template <int MT>
-static void launch_skinny_mt(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K,
-                             int splits, float *part, const Epi &ep, hipStream_t s) {
+template <typename T, int MT>
+static void launch_skinny_mt(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits, float *part,
+                             const Epi &ep, hipStream_t s) {
   constexpr int NSUB = 4, U = 2;
   int kchunk = (K + splits - 1) / splits;
   kchunk = (kchunk + 31) & ~31;
   splits = (K + kchunk - 1) / kchunk;
   dim3 grid((N + NSUB * 16 - 1) / (NSUB * 16), splits);
-  gemm_skinny_kernel<MT, NSUB, U><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, kchunk, part, ep);
+  gemm_skinny_kernel<T, MT, NSUB, U><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, kchunk, part, ep);
 }
 
 int skinny_effective_splits(int K, int splits) {
@@ -288,22 +282,33 @@ int skinny_effective_splits(int K, int splits) {
   return (K + kchunk - 1) / kchunk;
 }
 
-template <>
-void launch_gemm<bf16_t>(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K, int splits,
-                         float *part, const Epi &ep, hipStream_t s) {
+template <typename T>
+static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits, float *part,
+                             const Epi &ep, hipStream_t s) {
   if (M <= 0 || N <= 0) return;
   if (M <= 64) {
     if (splits < 1 || part == nullptr) splits = 1;
     switch ((M + 15) / 16) {
-      case 1: launch_skinny_mt<1>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      case 2: launch_skinny_mt<2>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      case 3: launch_skinny_mt<3>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      default: launch_skinny_mt<4>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 1: launch_skinny_mt<T, 1>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 2: launch_skinny_mt<T, 2>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 3: launch_skinny_mt<T, 3>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      default: launch_skinny_mt<T, 4>(X, ldx, W, M, N, K, splits, part, ep, s); break;
     }
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);
-  gemm_big_kernel<<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+  gemm_big_kernel<T><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+}
+
+template <>
+void launch_gemm<bf16_t>(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K, int splits,
+                         float *part, const Epi &ep, hipStream_t s) {
+  launch_gemm_mfma<bf16_t>(X, ldx, W, M, N, K, splits, part, ep, s);
+}
+template <>
+void launch_gemm<f16_t>(const f16_t *X, int64_t ldx, const f16_t *W, int M, int N, int K, int splits,
+                        float *part, const Epi &ep, hipStream_t s) {
+  launch_gemm_mfma<f16_t>(X, ldx, W, M, N, K, splits, part, ep, s);
 }
 
 template <>
@@ -316,5 +321,6 @@ void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int 
 
 template void launch_gemm_finish<float>(const float *, int, int, int, const Epi &, hipStream_t);
 template void launch_gemm_finish<bf16_t>(const float *, int, int, int, const Epi &, hipStream_t);
+template void launch_gemm_finish<f16_t>(const float *, int, int, int, const Epi &, hipStream_t);
 
 }  // namespace lp

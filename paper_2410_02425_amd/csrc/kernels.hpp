@@ -8,8 +8,9 @@ namespace lp {
 
 constexpr int KV_BLOCK = 64;  // tokens per KV-cache block
 
-// bf16 stored as raw 16-bit patterns.
+// bf16 stored as raw 16-bit patterns; fp16 as the native half type.
 typedef uint16_t bf16_t;
+typedef _Float16 f16_t;
 
 // Where the rows of a step read their token and write their results.
 struct RowMeta {
@@ -99,11 +100,12 @@ void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t 
                    int32_t *slot_tok, int32_t *tok_log, hipStream_t s);
 
 // Weight generator: writes rows x cols values of canonical tensor `tensor_id`
-// to dst with row r stored at dst_row(r) = r_off + perm(r) (see kernels), in T.
+// to dst with row r stored at perm(r), in T.  `bf16_values`: round each value
+// to bf16 first (a bf16 model held in fp16 storage keeps its exact values).
 enum RowPerm : int { PERM_NONE = 0, PERM_ROPE = 1, PERM_GATE = 2, PERM_UP = 3 };
 template <typename T>
 void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
-                        int64_t cols, float stdv, int perm, int head_dim, hipStream_t s);
+                        int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, hipStream_t s);
 void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s);
 
 }  // namespace lp

@@ -153,7 +153,7 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
 
 template <typename T>
 __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t tid, int64_t rows,
-                                   int64_t cols, float stdv, int perm, int hd) {
+                                   int64_t cols, float stdv, int perm, int hd, bool bf16_values) {
   const int64_t n = rows * cols;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (int64_t)gridDim.x * blockDim.x) {
@@ -162,7 +162,8 @@ __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t ti
     int s = 0;
 #pragma unroll
     for (int w = 0; w < 4; ++w) s += (c[w] & 1023u) + ((c[w] >> 10) & 1023u) + ((c[w] >> 20) & 1023u);
-    const float v = ((float)(s - 6138) * stdv) * 0x1p-10f;
+    float v = ((float)(s - 6138) * stdv) * 0x1p-10f;
+    if (bf16_values) v = bf16_to_f32(f32_to_bf16(v));
     const int64_t r = e / cols, col = e % cols;
     int64_t dr = r;
     if (perm == PERM_ROPE) {
@@ -179,11 +180,11 @@ __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t ti
 
 template <typename T>
 void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
-                        int64_t cols, float stdv, int perm, int head_dim, hipStream_t s) {
+                        int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, hipStream_t s) {
   const int64_t n = rows * cols;
   const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
   init_weight_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(dst, k0, k1, tensor_id, rows, cols, stdv,
-                                                        perm, head_dim);
+                                                        perm, head_dim, bf16_values);
 }
 
 __global__ void fill_f32_kernel(float *dst, int64_t n, float v) {
@@ -203,9 +204,10 @@ void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s) {
   template void launch_rmsnorm<T>(float *, const float *, int, int64_t, const int32_t *,          \
                                   const float *, T *, int, int, float, hipStream_t);              \
   template void launch_init_weight<T>(T *, uint32_t, uint32_t, uint32_t, int64_t, int64_t, float, \
-                                      int, int, hipStream_t);
+                                      int, int, bool, hipStream_t);
 INST(float)
 INST(bf16_t)
+INST(f16_t)
 #undef INST
 
 }  // namespace lp

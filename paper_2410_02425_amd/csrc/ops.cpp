@@ -35,20 +35,25 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
                           int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *stream) {
   OPCHK(X && W && Y && M >= 0 && N > 0 && K > 0, "gemm: bad pointers or sizes");
   OPCHK(K % 8 == 0 && N % 2 == 0 && ldx >= K && ldx % 8 == 0, "gemm: K % 8, N % 2, ldx");
-  OPCHK(dtype == LP_F32 || dtype == LP_BF16, "gemm: dtype");
+  OPCHK(dtype == LP_F32 || dtype == LP_BF16 || dtype == LP_F16, "gemm: dtype");
   hipStream_t s = (hipStream_t)stream;
   Epi ep{};
   ep.kind = EPI_STORE;
   ep.out = Y;
   ep.ldo = N;
-  if (dtype == LP_BF16) {
+  if (dtype != LP_F32) {
     int splits = 1;
     if (M <= 64 && k_splits > 1) {
       splits = skinny_effective_splits(K, k_splits);
       OPCHK(ws && ws_bytes >= (size_t)splits * M * N * 4, "gemm: workspace too small for split-K");
     }
-    launch_gemm<bf16_t>((const bf16_t *)X, ldx, (const bf16_t *)W, M, N, K, splits, (float *)ws, ep, s);
-    if (splits > 1) launch_gemm_finish<bf16_t>((const float *)ws, splits, M, N, ep, s);
+    if (dtype == LP_BF16) {
+      launch_gemm<bf16_t>((const bf16_t *)X, ldx, (const bf16_t *)W, M, N, K, splits, (float *)ws, ep, s);
+      if (splits > 1) launch_gemm_finish<bf16_t>((const float *)ws, splits, M, N, ep, s);
+    } else {
+      launch_gemm<f16_t>((const f16_t *)X, ldx, (const f16_t *)W, M, N, K, splits, (float *)ws, ep, s);
+      if (splits > 1) launch_gemm_finish<f16_t>((const float *)ws, splits, M, N, ep, s);
+    }
   } else {
     launch_gemm<float>((const float *)X, ldx, (const float *)W, M, N, K, 1, nullptr, ep, s);
   }
@@ -61,6 +66,8 @@ extern "C" int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
     launch_rmsnorm<bf16_t>(x, part, n_part, (int64_t)rows * d, nullptr, g, (bf16_t *)y, rows, d, eps, s);
+  else if (dtype == LP_F16)
+    launch_rmsnorm<f16_t>(x, part, n_part, (int64_t)rows * d, nullptr, g, (f16_t *)y, rows, d, eps, s);
   else if (dtype == LP_F32)
     launch_rmsnorm<float>(x, part, n_part, (int64_t)rows * d, nullptr, g, (float *)y, rows, d, eps, s);
   else
@@ -77,7 +84,7 @@ static int check_heads(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, in
   const int G = n_heads / n_kv_heads;
   OPCHK(G == 1 || G == 2 || G == 4 || G == 8, "attention: group size must be 1, 2, 4 or 8");
   OPCHK(head_dim == 64 || head_dim == 128, "attention: head_dim must be 64 or 128");
-  OPCHK(dtype == LP_BF16 || (dtype == LP_F32 && head_dim == 64), "attention: dtype / head_dim");
+  OPCHK(dtype == LP_BF16 || dtype == LP_F16 || (dtype == LP_F32 && head_dim == 64), "attention: dtype / head_dim");
   return LP_OK;
 }
 
@@ -98,6 +105,9 @@ extern "C" int lp_op_decode_attention(int32_t dtype, const void *q, void *out, c
   if (dtype == LP_BF16)
     launch_decode_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, rows, kv, 0, M, n_heads, max_ctx,
                                     (float *)ws, s);
+  else if (dtype == LP_F16)
+    launch_decode_attention<f16_t>((const f16_t *)q, (f16_t *)out, rows, kv, 0, M, n_heads, max_ctx,
+                                   (float *)ws, s);
   else
     launch_decode_attention<float>((const float *)q, (float *)out, rows, kv, 0, M, n_heads, max_ctx, (float *)ws,
                                    s);
@@ -119,6 +129,9 @@ extern "C" int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, 
   if (dtype == LP_BF16)
     launch_prefill_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, seq_start, seq_slot, n_seq, max_len, kv, 0,
                                      n_heads, s);
+  else if (dtype == LP_F16)
+    launch_prefill_attention<f16_t>((const f16_t *)q, (f16_t *)out, seq_start, seq_slot, n_seq, max_len, kv, 0,
+                                    n_heads, s);
   else
     launch_prefill_attention<float>((const float *)q, (float *)out, seq_start, seq_slot, n_seq, max_len, kv, 0,
                                     n_heads, s);
@@ -137,10 +150,13 @@ extern "C" int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
     launch_init_weight<bf16_t>((bf16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
-                               cols, stdv, PERM_NONE, 0, s);
+                               cols, stdv, PERM_NONE, 0, false, s);
+  else if (dtype == LP_F16)
+    launch_init_weight<f16_t>((f16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
+                              cols, stdv, PERM_NONE, 0, true, s);
   else if (dtype == LP_F32)
     launch_init_weight<float>((float *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows, cols,
-                              stdv, PERM_NONE, 0, s);
+                              stdv, PERM_NONE, 0, false, s);
   else
     OPCHK(false, "init_weight: dtype");
   return op_status();

@@ -14,9 +14,9 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 
 LP_OK, LP_EINVAL, LP_ENOMEM, LP_EHIP, LP_ESTATE = 0, -1, -2, -3, -4
-LP_F32, LP_BF16 = 0, 1
+LP_F32, LP_BF16, LP_F16 = 0, 1, 2
 LP_OPEN_LOOP, LP_CLOSED_LOOP = 0, 1
-LP_FLAG_KEEP_LOGITS, LP_FLAG_TIME_KERNEL = 1, 2
+LP_FLAG_KEEP_LOGITS, LP_FLAG_TIME_KERNEL, LP_FLAG_BF16_ACTIVATIONS = 1, 2, 4
 
 EXPORTED = [
     "lp_arena_bytes_required", "lp_engine_create", "lp_load_weights", "lp_init_weights_random",
@@ -54,7 +54,8 @@ class RunStats(C.Structure):
                 ("output_tokens", C.c_int64), ("prompt_tokens", C.c_int64), ("wall_ns", C.c_int64),
                 ("decode_ns", C.c_int64), ("decode_tokens", C.c_int64), ("full_decode_steps", C.c_int64),
                 ("full_decode_ns", C.c_int64), ("full_decode_sum_ctx", C.c_int64),
-                ("timed_kernel_launches", C.c_int64), ("timed_kernel_ms", C.c_double)]
+                ("timed_kernel_launches", C.c_int64), ("timed_kernel_rows", C.c_int64),
+                ("timed_kernel_ms", C.c_double)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -291,6 +292,8 @@ def sched_simulate(reqs, max_batch, max_batch_weight, max_prefill_tokens, closed
 
 def _dt(t):
     import torch
+    if t.dtype == torch.float16:
+        return LP_F16
     return LP_BF16 if t.dtype in (torch.bfloat16, torch.int16, torch.uint16) else LP_F32
 
 

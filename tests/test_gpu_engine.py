@@ -26,6 +26,8 @@ def cfg_dict(shape):
 
 
 def engine_for(shape, max_batch, max_seq, flags=lp.LP_FLAG_KEEP_LOGITS, max_prefill=4096, weight=0):
+    """Engine for `shape`; bf16 models compute with fp16 GEMM inputs unless
+    flags has LP_FLAG_BF16_ACTIVATIONS."""
     cfg = lp.make_config(shape)
     opt = lp.EngineOptions(max_batch, max_seq, weight, max_prefill, 0, flags)
     return lp.Engine(cfg, opt)
@@ -124,12 +126,20 @@ def test_tiny_open_loop_replay():
         np.testing.assert_array_equal(eng.result(r.id)["tokens"], T.generate(m, r.prompt, r.out_len)[0])
 
 
-def test_tiny_bf16_teacher_forced_logits():
+# Logit tolerance of the bf16 model path.  fp16 GEMM inputs / KV cache: the
+# stated 2e-2.  bf16 GEMM inputs / KV cache: rounding 8x coarser; replaying the
+# bf16 rounding points in float64 on the 2-layer 8B-shape case gives 5.2e-2,
+# so that mode is held to 8e-2.
+TOL = {0: 2e-2, lp.LP_FLAG_BF16_ACTIVATIONS: 8e-2}
+
+
+@pytest.mark.parametrize("act", [0, lp.LP_FLAG_BF16_ACTIVATIONS])
+def test_tiny_bf16_teacher_forced_logits(act):
     shape = synth.ModelShape("tiny-bf16", 2, 256, 4, 4, 688, 1024)
     w = synth.model_weights(shape, 11)
     rng = np.random.default_rng(2)
     reqs = [synth.Request(i, rng.integers(0, 1024, size=n).astype(np.int32), 6) for i, n in enumerate([32, 1, 70])]
-    eng = engine_for(shape, 4, 96)
+    eng = engine_for(shape, 4, 96, flags=lp.LP_FLAG_KEEP_LOGITS | act)
     eng.load_weights(synth.weights_blob(shape, w))
     eng.submit(reqs)
     m = T.Model(cfg_dict(shape), w)
@@ -141,10 +151,11 @@ def test_tiny_bf16_teacher_forced_logits():
     eng.run(lp.LP_CLOSED_LOOP, 4)
     for r in reqs:
         got = np.stack([eng.logits(r.id, k) for k in range(r.out_len)])
-        assert np.max(np.abs(got - ref[r.id])) <= 2e-2
+        assert np.max(np.abs(got - ref[r.id])) <= TOL[act]
 
 
-def test_8b_shape_two_layers_full_width_teacher_forced():
+@pytest.mark.parametrize("act", [0, lp.LP_FLAG_BF16_ACTIVATIONS])
+def test_8b_shape_two_layers_full_width_teacher_forced(act):
     """8B-shape GQA at full width (d=4096, 32/8 heads, F=14336, V=128256),
     2 layers, device-generated weights; logits compared on 2048 sampled vocab
     rows plus the GPU's argmax (teacher forcing keeps both on one sequence)."""
@@ -155,7 +166,7 @@ def test_8b_shape_two_layers_full_width_teacher_forced():
             synth.Request(1, rng.integers(0, shape.vocab, size=1).astype(np.int32), 3),
             synth.Request(2, rng.integers(0, shape.vocab, size=300).astype(np.int32), 2)]
     forced = {0: [5, 127000], 1: [99, 1], 2: [42]}
-    eng = engine_for(shape, 4, 512, max_prefill=1024)
+    eng = engine_for(shape, 4, 512, flags=lp.LP_FLAG_KEEP_LOGITS | act, max_prefill=1024)
     eng.init_weights_random(seed, 0.02)
     eng.submit(reqs)
     for r in reqs:
@@ -188,7 +199,7 @@ def test_8b_shape_two_layers_full_width_teacher_forced():
         got = got_all[r.id][:, rows_needed]
         err = np.max(np.abs(got - ref))
         print(f"request {r.id}: max |logit error| on {rows_needed.size} rows = {err:.3e}")
-        assert err <= 2e-2
+        assert err <= TOL[act]
         # the GPU's greedy choice is (within tolerance) the oracle's best among the sampled rows
         pos = np.searchsorted(rows_needed, gpu_top[r.id])
-        assert np.all(ref[np.arange(len(pos)), pos] >= ref.max(axis=1) - 4e-2)
+        assert np.all(ref[np.arange(len(pos)), pos] >= ref.max(axis=1) - 2 * TOL[act])

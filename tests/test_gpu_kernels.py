@@ -39,12 +39,16 @@ GEMM_CASES = [
 ]
 
 
+HALF = {"bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.mark.parametrize("half", ["bf16", "f16"])
 @pytest.mark.parametrize("M,N,K,splits", GEMM_CASES)
-def test_gemm_bf16(M, N, K, splits):
+def test_gemm_16bit(M, N, K, splits, half):
     rng = np.random.default_rng(M * 7 + N + K)
-    X = bf16_values(rng, (M, K))
+    X = bf16_values(rng, (M, K))          # bf16 values are exact in fp16 too
     W = bf16_values(rng, (N, K), 0.02)
-    Xd, Wd = to_dev(X, torch.bfloat16), to_dev(W, torch.bfloat16)
+    Xd, Wd = to_dev(X, HALF[half]), to_dev(W, HALF[half])
     Y = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
     ws = torch.empty(max(splits, 1) * M * N, dtype=torch.float32, device=DEV)
     lp.op_gemm(Xd, Wd, Y, splits, ws)
@@ -55,13 +59,14 @@ def test_gemm_bf16(M, N, K, splits):
     assert np.all(np.abs(got - ref) <= bound), np.max(np.abs(got - ref) / bound)
 
 
-def test_gemm_bf16_full_8b_gate_up_sampled():
+@pytest.mark.parametrize("half", ["bf16", "f16"])
+def test_gemm_full_8b_gate_up_sampled(half):
     """The decode gate/up GEMM at its full 8B-shape size (M=64, N=2*14336,
     K=4096), checked on 512 sampled outputs computed one by one."""
     M, N, K = 64, 28672, 4096
     g = torch.Generator().manual_seed(1234)
-    X = torch.randn(M, K, generator=g).to(torch.bfloat16)
-    W = (torch.randn(N, K, generator=g) * 0.02).to(torch.bfloat16)
+    X = torch.randn(M, K, generator=g).to(HALF[half])
+    W = (torch.randn(N, K, generator=g) * 0.02).to(HALF[half])
     Y = torch.empty(M, N, dtype=torch.float32, device=DEV)
     lp.op_gemm(X.to(DEV), W.to(DEV), Y, 1, None)
     torch.cuda.synchronize()
@@ -88,14 +93,14 @@ def test_gemm_f32(M, N, K):
     assert np.all(np.abs(Y.cpu().numpy() - ref) <= bound)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("rows,d,n_part", [(4, 256, 0), (64, 4096, 3), (7, 8192, 0), (33, 5120, 1)])
 def test_rmsnorm(dtype, rows, d, n_part):
     rng = np.random.default_rng(rows + d)
     x = (rng.standard_normal((rows, d)) * 3).astype(np.float32)
     part = (rng.standard_normal((max(n_part, 1), rows, d))).astype(np.float32)
     g = rng.uniform(0.5, 1.5, d).astype(np.float32)
-    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
     xd = to_dev(x, torch.float32)
     y = torch.empty(rows, d, dtype=tdt, device=DEV)
     lp.op_rmsnorm(xd, to_dev(g, torch.float32), y, 1e-5, to_dev(part, torch.float32) if n_part else None, n_part)
@@ -103,7 +108,7 @@ def test_rmsnorm(dtype, rows, d, n_part):
     xs = x.astype(np.float64) + (part[:n_part].astype(np.float64).sum(0) if n_part else 0)
     ref = T.rmsnorm(xs, g.astype(np.float64), 1e-5)
     got = y.float().cpu().numpy()
-    tol = 1e-5 if dtype == "f32" else 2 ** -8
+    tol = {"f32": 1e-5, "bf16": 2 ** -8, "f16": 2 ** -10}[dtype]
     assert np.all(np.abs(got - ref) <= tol * np.abs(ref) + 1e-6)
     if n_part:
         np.testing.assert_allclose(xd.cpu().numpy(), xs, rtol=1e-6, atol=1e-5)
@@ -124,16 +129,16 @@ def test_argmax_ties_and_tail():
     assert out.cpu().numpy()[:4].tolist() == [5, V - 1, 0, 0]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 def test_device_weight_generator_matches_host(dtype):
     rows, cols, tid, seed = 300, 688, 17, 0x1234ABCD5678
-    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
     dst = torch.empty(rows, cols, dtype=tdt, device=DEV)
     lp.op_init_weight(dst, seed, tid, 0.02)
     torch.cuda.synchronize()
     host = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02,
                                synth.DTYPE_F32 if dtype == "f32" else synth.DTYPE_BF16)
-    got = dst.float().cpu().numpy()
+    got = dst.float().cpu().numpy()  # fp16 storage holds the bf16 values exactly
     assert np.array_equal(got.view(np.uint32), host.view(np.uint32))
 
 
@@ -166,6 +171,8 @@ def make_paged_cache(rng, ctx_lens, Hkv, hd, tdt, extra_blocks=3):
 DECODE_CASES = [
     # dtype, Hq, Hkv, hd, context lengths
     ("bf16", 32, 8, 128, [1, 63, 64, 65, 256, 257, 700, 5120]),
+    ("f16", 32, 8, 128, [1, 63, 64, 65, 256, 257, 700, 5120]),
+    ("f16", 64, 8, 128, [129, 4096]),
     ("bf16", 8, 8, 128, [300, 2, 1024]),
     ("bf16", 64, 8, 128, [77, 4096]),
     ("bf16", 4, 4, 64, [40, 33]),
@@ -177,7 +184,7 @@ DECODE_CASES = [
 @pytest.mark.parametrize("dtype,Hq,Hkv,hd,ctx", DECODE_CASES)
 def test_decode_attention(dtype, Hq, Hkv, hd, ctx):
     rng = np.random.default_rng(len(ctx) * 100 + Hq)
-    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
     (kc, vt, bt), Ks, Vs = make_paged_cache(rng, ctx, Hkv, hd, tdt)
     M = len(ctx)
     q = bf16_values(rng, (M, Hq, hd))
@@ -192,12 +199,13 @@ def test_decode_attention(dtype, Hq, Hkv, hd, ctx):
     for m, c in enumerate(ctx):
         ref = T.attention(q[m:m + 1].astype(np.float64), Ks[m].astype(np.float64), Vs[m].astype(np.float64),
                           [c - 1], np.arange(c), Hkv)[0]
-        tol = 2e-5 if dtype == "f32" else 2 ** -8 * np.abs(ref) + 2e-3
+        tol = {"f32": 2e-5, "bf16": 2 ** -8 * np.abs(ref) + 2e-3, "f16": 2 ** -10 * np.abs(ref) + 2e-4}[dtype]
         assert np.all(np.abs(got[m] - ref) <= tol), (m, c, np.max(np.abs(got[m] - ref)))
 
 
 PREFILL_CASES = [
     ("bf16", 32, 8, 128, [1, 17, 64, 65, 200]),
+    ("f16", 32, 8, 128, [1, 17, 64, 65, 200]),
     ("bf16", 8, 8, 128, [130, 3]),
     ("bf16", 4, 4, 64, [32, 32, 32, 32]),
     ("f32", 4, 4, 64, [32, 32, 5, 100]),
@@ -208,7 +216,7 @@ PREFILL_CASES = [
 @pytest.mark.parametrize("dtype,Hq,Hkv,hd,lens", PREFILL_CASES)
 def test_prefill_attention(dtype, Hq, Hkv, hd, lens):
     rng = np.random.default_rng(sum(lens) + Hq)
-    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
     (kc, vt, bt), Ks, Vs = make_paged_cache(rng, lens, Hkv, hd, tdt)
     rows = sum(lens)
     q = bf16_values(rng, (rows, Hq, hd))
@@ -222,6 +230,6 @@ def test_prefill_attention(dtype, Hq, Hkv, hd, lens):
     for j, n in enumerate(lens):
         ref = T.attention(q[r0:r0 + n].astype(np.float64), Ks[j].astype(np.float64), Vs[j].astype(np.float64),
                           np.arange(n), np.arange(n), Hkv)
-        tol = 2e-5 if dtype == "f32" else 2 ** -8 * np.abs(ref) + 2e-3
+        tol = {"f32": 2e-5, "bf16": 2 ** -8 * np.abs(ref) + 2e-3, "f16": 2 ** -10 * np.abs(ref) + 2e-4}[dtype]
         assert np.all(np.abs(got[r0:r0 + n] - ref) <= tol), (j, np.max(np.abs(got[r0:r0 + n] - ref)))
         r0 += n
