@@ -12,6 +12,8 @@
 
 namespace lp {
 
+typedef unsigned int u32x4_tt __attribute__((ext_vector_type(4)));
+
 constexpr int DEC_CHUNK = 256;  // positions per decode workgroup
 constexpr int MAX_GROUP = 8;    // query heads per kv head
 
@@ -180,6 +182,157 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
   out[((int64_t)m * n_heads + h) * HD + c] = Act<T>::st(num / den);
 }
 
+// 16-bit decode attention on MFMA.  One wave owns one 64-position KV block:
+// S = Q K^T is four 16x16 tiles (query heads of the group padded to 16 rows,
+// positions as columns, head_dim as the contraction), the softmax is reduced
+// across the 16 lanes that hold a row, P goes through LDS into the A-operand
+// layout, and O = P V contracts over positions with V read from its
+// transposed [hd][64] block as 16-byte B fragments.  All K and V fragments
+// of the block are requested before any is used.
+template <typename T, int HD, int G>
+__global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restrict__ q, RowMeta rows, KVCache kv,
+                                                               int layer, int n_heads, int max_splits,
+                                                               float *__restrict__ ws) {
+  typedef typename Mfma<T>::v8 v8;
+  constexpr int KS = HD / 32;  // contraction steps over head_dim
+  constexpr int NT = HD / 16;  // 16-wide output tiles over head_dim
+  __shared__ T pls[4][16][64 + 8];
+  __shared__ float wm[4][16], wl[4][16];
+  __shared__ float wo[4][G][HD];
+  const int s = blockIdx.x, g = blockIdx.y, m = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, quad = lane >> 4, kq = quad * 8;
+  const int slot = rows.row_slot[m];
+  const int ctx = rows.row_pos[m] + 1;
+  if (s * DEC_CHUNK >= ctx) return;
+  const int blk_pos = s * DEC_CHUNK + wave * 64;
+  const int nvalid = max(0, min(64, ctx - blk_pos));
+
+  v8 qa[KS];
+  const T *qrow = q + ((int64_t)m * n_heads + g * G + (r16 < G ? r16 : 0)) * HD;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qa[ks] = (r16 < G) ? load8<T>(qrow + ks * 32 + kq) : zero8<T>();
+
+  v8 kf[4][KS], vf[NT][2];
+  if (nvalid > 0) {
+    const int64_t base = kv_block_base(kv, layer, slot, blk_pos, g);
+    const T *kb = (const T *)kv.k + base;
+    const T *vb = (const T *)kv.v + base;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) vf[nt][kk] = load8<T>(vb + (nt * 16 + r16) * KV_BLOCK + kk * 32 + kq);
+  } else {
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = zero8<T>();
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) vf[nt][0] = vf[nt][1] = zero8<T>();
+  }
+  // positions past the context hold stale or uninitialised cache entries
+  if (nvalid < 64) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kk * 32 + kq + e >= nvalid) vf[nt][kk][e] = (typename Mfma<T>::v8){}[0];
+  }
+
+  floatx4_t sacc[4];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) {
+    sacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) sacc[nt] = Mfma<T>::m16(qa[ks], kf[nt][ks], sacc[nt]);
+  }
+  // sacc[nt][i]: row (head) 4*quad + i, position nt*16 + r16
+  const float scale = rsqrtf((float)HD);
+  float mx[4], sm[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float v = -INFINITY;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const bool ok = nt * 16 + r16 < nvalid;
+      sacc[nt][i] = ok ? sacc[nt][i] * scale : -INFINITY;
+      v = fmaxf(v, sacc[nt][i]);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    mx[i] = v;
+    float t = 0.f;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const float p = (v == -INFINITY) ? 0.f : __expf(sacc[nt][i] - v);
+      sacc[nt][i] = p;
+      t += p;
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) t += __shfl_xor(t, o, 64);
+    sm[i] = t;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) pls[wave][4 * quad + i][nt * 16 + r16] = Act<T>::st(sacc[nt][i]);
+  }
+  __syncthreads();
+  v8 pa[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) pa[kk] = load8<T>(&pls[wave][r16][kk * 32 + kq]);
+  floatx4_t oacc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    oacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) oacc[nt] = Mfma<T>::m16(pa[kk], vf[nt][kk], oacc[nt]);
+  }
+  if (r16 == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      wm[wave][4 * quad + i] = mx[i];
+      wl[wave][4 * quad + i] = sm[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * quad + i;
+    if (h < G) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) wo[wave][h][nt * 16 + r16] = oacc[nt][i];
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * (HD + 2); e += 256) {
+    const int h = e / (HD + 2), c = e % (HD + 2);
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, wm[w][h]);
+    float acc = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (wm[w][h] == -INFINITY) continue;
+      const float f = __expf(wm[w][h] - M);
+      acc += f * (c < HD ? wo[w][h][c] : wl[w][h]);
+    }
+    float *dst = ws + (((int64_t)m * n_heads + g * G + h) * max_splits + s) * (HD + 2);
+    dst[c] = (c == HD) ? M : acc;  // [0, HD): output, HD: max, HD + 1: sum
+  }
+}
+
+template <typename T, int HD, int G>
+static void launch_decode_group(dim3 grid, const T *q, const RowMeta &rows, const KVCache &kv, int layer,
+                                int n_heads, int splits, float *ws, hipStream_t s) {
+  if constexpr (sizeof(T) == 2)
+    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws);
+  else
+    decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws);
+}
+
 template <typename T, int HD>
 static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
                              int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
@@ -187,10 +340,10 @@ static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCa
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
   dim3 grid(splits, kv.n_kv_heads, M);
   switch (G) {
-    case 1: decode_attn_kernel<T, HD, 1><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
-    case 2: decode_attn_kernel<T, HD, 2><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
-    case 4: decode_attn_kernel<T, HD, 4><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
-    case 8: decode_attn_kernel<T, HD, 8><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws); break;
+    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
+    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
+    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
+    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
     default: return;
   }
   decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, splits, ws, out);
@@ -274,6 +427,169 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(const T *__restrict__
   }
 }
 
+// 16-bit causal prefill attention on MFMA (flash-attention style).  A
+// workgroup owns 64 query rows of one (sequence, head); each wave owns 16 of
+// them.  Key blocks of 64 positions are staged in LDS (K as [key][dim], V
+// transposed as [dim][key], rows padded so the 16-byte fragment reads of a
+// wave fall in distinct banks) with the next block prefetched into registers
+// while the current one is used.  S = Q K^T and O += P V are 16x16x32 MFMAs,
+// the softmax is online (running max and sum per row), and only the diagonal
+// block needs the causal mask.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void prefill_attn_mfma_kernel(const T *__restrict__ q, T *__restrict__ out,
+                                                                const int32_t *seq_start, const int32_t *seq_slot,
+                                                                KVCache kv, int layer, int n_heads) {
+  typedef typename Mfma<T>::v8 v8;
+  constexpr int KS = HD / 32;                 // contraction steps over head_dim
+  constexpr int NT = HD / 16;                 // output tiles over head_dim
+  constexpr int KPAD = HD + 8;                // K row stride (elements)
+  constexpr int VPAD = 64 + 8;                // Vt row stride
+  constexpr int CH = 64 * HD * 2 / 16 / 256;  // 16-byte chunks per thread per block (K and V)
+  __shared__ T ks[64][KPAD];
+  __shared__ T vs[HD][VPAD];
+  __shared__ T pls[4][16][64 + 8];
+  const int qt = blockIdx.x, h = blockIdx.y, j = blockIdx.z;
+  const int row0 = seq_start[j];
+  const int len = seq_start[j + 1] - row0;
+  if (qt * 64 >= len) return;
+  const int slot = seq_slot[j];
+  const int g = h / (n_heads / kv.n_kv_heads);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, quad = lane >> 4, kq = quad * 8;
+  const int q0 = qt * 64 + wave * 16;  // first query position of this wave
+
+  v8 qa[KS];
+  {
+    const int qp = min(q0 + r16, len - 1);
+    const T *qr = q + ((int64_t)(row0 + qp) * n_heads + h) * HD;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) qa[k] = load8<T>(qr + k * 32 + kq);
+  }
+  floatx4_t oacc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) oacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float mrow[4], lrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    mrow[i] = -INFINITY;
+    lrow[i] = 0.f;
+  }
+  const float scale = rsqrtf((float)HD);
+  const int nblk = min(qt + 1, (len + 63) / 64);  // causal: key blocks up to the diagonal
+
+  // staging: chunk c of a block -> K: key c / (HD/8), dims (c % (HD/8)) * 8;
+  //                               Vt: dim c / 8, keys (c % 8) * 8
+  u32x4_tt kr[CH], vr[CH];
+  auto fetch = [&](int kb) __attribute__((always_inline)) {
+    const int64_t base = kv_block_base(kv, layer, slot, kb * 64, g);
+    const u32x4_tt *kp = (const u32x4_tt *)((const T *)kv.k + base);
+    const u32x4_tt *vp = (const u32x4_tt *)((const T *)kv.v + base);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      kr[c] = kp[tid + c * 256];
+      vr[c] = vp[tid + c * 256];
+    }
+  };
+  fetch(0);
+  for (int kb = 0; kb < nblk; ++kb) {
+    __syncthreads();  // previous block fully consumed
+    const int kvalid = len - kb * 64;  // keys of this block inside the sequence
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int e = tid + c * 256;
+      *(u32x4_tt *)&ks[e / (HD / 8)][(e % (HD / 8)) * 8] = kr[c];
+      // cache entries past the sequence end are stale or uninitialised; their
+      // softmax weight is 0 but 0 * NaN is not, so they become zeros here
+      u32x4_tt v = vr[c];
+      const int key0 = (e % 8) * 8;
+      if (key0 + 8 > kvalid) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t lo = key0 + 2 * w < kvalid ? 0xFFFFu : 0u;
+          const uint32_t hi = key0 + 2 * w + 1 < kvalid ? 0xFFFF0000u : 0u;
+          v[w] &= (lo | hi);
+        }
+      }
+      *(u32x4_tt *)&vs[e / 8][key0] = v;
+    }
+    __syncthreads();
+    if (kb + 1 < nblk) fetch(kb + 1);
+    // S = Q K^T over the 64 keys of this block
+    floatx4_t sacc[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      sacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < KS; ++k) sacc[nt] = Mfma<T>::m16(qa[k], load8<T>(&ks[nt * 16 + r16][k * 32 + kq]), sacc[nt]);
+    }
+    // online softmax: row 4*quad + i of this wave, keys nt*16 + r16
+    const bool diag = kb == nblk - 1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int qpos = q0 + 4 * quad + i;
+      float mx = mrow[i];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int kpos = kb * 64 + nt * 16 + r16;
+        const bool ok = !diag || (kpos <= qpos && kpos < len);
+        sacc[nt][i] = ok ? sacc[nt][i] * scale : -INFINITY;
+        mx = fmaxf(mx, sacc[nt][i]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      // rows past the sequence end see no valid key: keep them finite
+      const float mref = (mx == -INFINITY) ? 0.f : mx;
+      const float corr = __expf(mrow[i] - mref);
+      float t = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const float p = __expf(sacc[nt][i] - mref);
+        sacc[nt][i] = p;
+        t += p;
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) t += __shfl_xor(t, o, 64);
+      lrow[i] = lrow[i] * corr + t;
+      mrow[i] = mx;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) oacc[nt][i] *= corr;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) pls[wave][4 * quad + i][nt * 16 + r16] = Act<T>::st(sacc[nt][i]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    v8 pa[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) pa[kk] = load8<T>(&pls[wave][r16][kk * 32 + kq]);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        oacc[nt] = Mfma<T>::m16(pa[kk], load8<T>(&vs[nt * 16 + r16][kk * 32 + kq]), oacc[nt]);
+  }
+  // rows 4*quad + i, dims nt*16 + r16
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qpos = q0 + 4 * quad + i;
+    if (qpos < len) {
+      const float inv = 1.0f / lrow[i];
+      T *orow = out + ((int64_t)(row0 + qpos) * n_heads + h) * HD;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) orow[nt * 16 + r16] = Act<T>::st(oacc[nt][i] * inv);
+    }
+  }
+}
+
+template <typename T, int HD>
+static void launch_prefill_hd(dim3 grid, const T *q, T *out, const int32_t *seq_start, const int32_t *seq_slot,
+                              const KVCache &kv, int layer, int n_heads, hipStream_t s) {
+  if constexpr (sizeof(T) == 2)
+    prefill_attn_mfma_kernel<T, HD><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+  else
+    prefill_attn_kernel<T, HD><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+}
+
 template <typename T>
 void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, const int32_t *seq_slot,
                               int n_seq, int max_len, const KVCache &kv, int layer, int n_heads,
@@ -281,9 +597,9 @@ void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, cons
   if (n_seq <= 0) return;
   dim3 grid((max_len + 63) / 64, n_heads, n_seq);
   if (kv.head_dim == 128)
-    prefill_attn_kernel<T, 128><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+    launch_prefill_hd<T, 128>(grid, q, out, seq_start, seq_slot, kv, layer, n_heads, s);
   else if (kv.head_dim == 64)
-    prefill_attn_kernel<T, 64><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+    launch_prefill_hd<T, 64>(grid, q, out, seq_start, seq_slot, kv, layer, n_heads, s);
 }
 
 #define INST(T)                                                                                     \

@@ -17,7 +17,7 @@
 #include "scheduler.hpp"
 
 namespace lp {
-int skinny_effective_splits(int K, int splits);
+int skinny_effective_splits(int N, int K, int splits);
 }
 
 using namespace lp;
@@ -77,11 +77,12 @@ Dims dims_of(const lp_model_config &c, uint32_t flags = 0) {
 int64_t rows_cap(const lp_engine_options &o) { return std::max<int64_t>(o.max_batch, o.max_prefill_tokens); }
 
 int decode_splits(int N, int K) {
-  // enough workgroups to cover the chip twice with 64-column tiles, chunks >= 256
-  const int tiles = (N + 63) / 64;
-  int s = std::max(1, (512 + tiles - 1) / tiles);
-  s = std::min(s, std::max(1, K / 256));
-  return lp::skinny_effective_splits(K, s);
+  // K splits of the decode GEMMs whose epilogue can be deferred: about four
+  // waves per CU (two 16-column slices per wave), with chunks of >= 512 k
+  const int waves_per_split = std::max(1, N / 32);
+  int s = std::max(1, (1024 + waves_per_split - 1) / waves_per_split);
+  s = std::min(s, std::max(1, K / 512));
+  return lp::skinny_effective_splits(N, K, s);
 }
 
 size_t part_bytes_for(const Dims &D, const lp_model_config &c, int max_batch) {
@@ -309,7 +310,7 @@ extern "C" int lp_engine_create(const lp_model_config *cfg, const lp_engine_opti
   hipError_t s = hipEventCreate(&e->ev_start);
   for (int i = 0; i < RING && s == hipSuccess; ++i) s = hipEventCreate(&e->ev_step[i]);
   if (s == hipSuccess && (opt->flags & LP_FLAG_TIME_KERNEL)) {
-    e->ev_kern.resize((size_t)RING * e->D.L * 2);
+    e->ev_kern.resize((size_t)RING * 2);
     for (auto &ev : e->ev_kern)
       if (s == hipSuccess) s = hipEventCreate(&ev);
   }
@@ -609,7 +610,11 @@ KVCache kv_of(lp_engine *e, const int32_t *block_table) {
 // lm_rows; decode: rows attend to their slots' caches.
 template <typename T>
 int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_len, const StepMeta &dm,
-               int64_t log_off, int step_ring) {
+               int64_t log_off, int64_t step) {
+  const int step_ring = (int)(step % RING);
+  // LP_FLAG_TIME_KERNEL: one layer's gate/up launch per decode step, rotating
+  // over the layers, is bracketed by events (each event adds a gap)
+  const int timed_layer = (int)(step % e->D.L);
   const Dims &D = e->D;
   hipStream_t st = e->stream;
   float *x = e->ptr<float>(e->Ly.x);
@@ -668,8 +673,8 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
     eg.act_out = hb;
     eg.ld_act = D.F;
     hipEvent_t *tk = nullptr;
-    if (!prefill && !e->ev_kern.empty()) {
-      tk = &e->ev_kern[((size_t)step_ring * D.L + l) * 2];
+    if (!prefill && !e->ev_kern.empty() && l == timed_layer) {
+      tk = &e->ev_kern[(size_t)step_ring * 2];
       hipEventRecord(tk[0], st);
     }
     launch_gemm<T>(xn, D.d, e->ptr<T>(e->Ly.wgu[l]), M, 2 * D.F, D.d, 1, part, eg, st);
@@ -710,8 +715,9 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
 }  // namespace
 
 // Issues one planned step; returns its tok_log offset via log_off.
-static int launch_step(lp_engine *e, const PlanStep &ps, int ring, int64_t log_off,
+static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t log_off,
                        const std::vector<int32_t> &block_table_host) {
+  const int ring = (int)(step % RING);
   const int M = ps.kind == 0 ? (int)ps.n_tokens : (int)ps.reqs.size();
   const int n_rows = (int)ps.reqs.size();
   int32_t *h = e->staging[ring];
@@ -765,16 +771,16 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int ring, int64_t log_o
   switch (e->D.act) {
     case ACT_F16:
       launch_embed<f16_t>(e->ptr<f16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
-      rc = run_layers<f16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+      rc = run_layers<f16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
       break;
     case ACT_BF16:
       launch_embed<bf16_t>(e->ptr<bf16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d,
                            e->stream);
-      rc = run_layers<bf16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+      rc = run_layers<bf16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
       break;
     default:
       launch_embed<float>(e->ptr<float>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
-      rc = run_layers<float>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, ring);
+      rc = run_layers<float>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
   }
   if (rc) return rc;
   HIPCHK(e, hipEventRecord(e->ev_step[ring], e->stream));
@@ -799,14 +805,12 @@ int read_step(lp_engine *e, RunState &rs, int64_t k) {
   const int64_t base = k == 0 ? 0 : rs.end_ns[k - 1];
   rs.end_ns[k] = base + (int64_t)std::llround((double)ms * 1e6);
   if (!e->ev_kern.empty() && e->steps[k].kind == 1) {
-    for (int l = 0; l < e->D.L; ++l) {
-      float km = 0.f;
-      hipEvent_t *tk = &e->ev_kern[((size_t)ring * e->D.L + l) * 2];
-      if (hipEventElapsedTime(&km, tk[0], tk[1]) == hipSuccess) {
-        e->stats.timed_kernel_ms += km;
-        e->stats.timed_kernel_launches += 1;
-        e->stats.timed_kernel_rows += e->steps[k].n_rows;
-      }
+    float km = 0.f;
+    hipEvent_t *tk = &e->ev_kern[(size_t)ring * 2];
+    if (hipEventElapsedTime(&km, tk[0], tk[1]) == hipSuccess) {
+      e->stats.timed_kernel_ms += km;
+      e->stats.timed_kernel_launches += 1;
+      e->stats.timed_kernel_rows += e->steps[k].n_rows;
     }
   }
   rs.read = k + 1;
@@ -885,7 +889,7 @@ extern "C" int lp_run(lp_engine *e, int32_t mode, int32_t concurrency) {
         int rc = read_step(e, rs, k - LOOKAHEAD);
         if (rc) return rc;
       }
-      int rc = launch_step(e, ps, (int)(k % RING), log_off, bt);
+      int rc = launch_step(e, ps, k, log_off, bt);
       if (rc) return rc;
       log_off += (int64_t)ps.reqs.size();
     }

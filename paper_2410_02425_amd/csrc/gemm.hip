@@ -8,98 +8,140 @@
 //    fp32 partials reduced by a finishing pass.
 //  * gemm_big: bf16 MFMA for prefill-sized M, 128x128x64 tiles staged in LDS.
 //  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
+#include <algorithm>
+
 #include "device.hpp"
 
 namespace lp {
 
 
 // ------------------------------------------------------------------ skinny (decode)
+//
+// Decode-sized M (<= 64 rows, MT 16-row tiles).  The weight stream is the whole
+// cost: each wave owns NS 16-row slices of W and streams them over the
+// workgroup's K range, one sub-chunk (KSUB 32-wide k-steps) ahead of the MFMAs.
+// The activations of a sub-chunk are staged once per workgroup into LDS in
+// MFMA-fragment order (one 1 KB block per (k-step, m-tile), lane-major), so
+// they never occupy the vector-memory counter the weight prefetch waits on.
+// The loop body has no exit between a prefetch and its use, and prefetches
+// past the end re-read the last sub-chunk, so the compiler's wait counts stay
+// exact.  Columns of the workgroup's chunk beyond K are zeroed in LDS; the
+// weight loads there read valid neighbouring memory and meet those zeros.
+// Each workgroup rotates its starting sub-chunk so that concurrent
+// workgroups spread over the K range.
 
-template <typename T, int MT, int NSUB, int U>
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(const T *__restrict__ X, int64_t ldx,
-                                                          const T *__restrict__ W, int M, int N,
-                                                          int K, int kchunk, float *__restrict__ part,
-                                                          Epi ep) {
-  constexpr int TILES = MT * NSUB;
-  __shared__ floatx4_t red[4][TILES][64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r16 = lane & 15, kq = (lane >> 4) * 8;
-  const int n0 = blockIdx.x * NSUB * 16;
-  const int s = blockIdx.y;
-  const int kbeg = s * kchunk;
-  const int kend = min(K, kbeg + kchunk);
-  const int kw = (((kend - kbeg + 3) / 4) + 31) & ~31;
-  const int kw0 = kbeg + wave * kw;
-  const int kw1 = min(kend, kw0 + kw);
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-  floatx4_t acc[MT][NSUB];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < NSUB; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
+template <typename T, int MT, int NS, int KSUB, int NW>
+__global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restrict__ X, int64_t ldx,
+                                                             const T *__restrict__ W, int M, int N, int K,
+                                                             int kchunk, float *__restrict__ part, Epi ep) {
   typedef typename Mfma<T>::v8 v8;
-  const T *wrow[NSUB];
-  bool nvalid[NSUB];
-#pragma unroll
-  for (int j = 0; j < NSUB; ++j) {
-    const int n = n0 + j * 16 + r16;
-    nvalid[j] = n < N;
-    wrow[j] = W + (int64_t)(nvalid[j] ? n : 0) * K;
-  }
-  const T *xrow[MT];
-  bool mvalid[MT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    const int m = i * 16 + r16;
-    mvalid[i] = m < M;
-    xrow[i] = X + (int64_t)(mvalid[i] ? m : 0) * ldx;
-  }
+  constexpr int KC = KSUB * 32;
+  constexpr int XT = KSUB * MT * 64;                     // fragment entries per sub-chunk
+  constexpr int XF = (XT + NW * 64 - 1) / (NW * 64);     // ... staged per thread
+  __shared__ u32x4_t xs0[KSUB][MT][64];
+  __shared__ u32x4_t xs1[KSUB][MT][64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  const int n0 = (blockIdx.x * NW + wave) * NS * 16;
+  const int kbeg = blockIdx.y * kchunk, kend = min(K, kbeg + kchunk);
+  const int nsub = ((kend - kbeg + 2 * KC - 1) / (2 * KC)) * 2;
+  const int rot = (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nsub);
+#define SK_SC(c) (kbeg + (((c) + rot) % nsub) * KC)
+  const int klast = SK_SC(nsub - 1);
 
-  for (int k = kw0; k < kw1; k += 32 * U) {
-    v8 a[U][MT], b[U][NSUB];
+  const T *wrow[NS];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kk = k + u * 32 + kq;
-      const bool kv = kk < kw1;
+  for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min(n0 + j * 16 + r16, N - 1) * K;
+  const T *xsrc[XF];
+  int xk[XF];
 #pragma unroll
-      for (int j = 0; j < NSUB; ++j) b[u][j] = (kv && nvalid[j]) ? load8<T>(wrow[j] + kk) : zero8<T>();
-#pragma unroll
-      for (int i = 0; i < MT; ++i) a[u][i] = (kv && mvalid[i]) ? load8<T>(xrow[i] + kk) : zero8<T>();
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NSUB; ++j)
-          acc[i][j] = Mfma<T>::m16(a[u][i], b[u][j], acc[i][j]);
+  for (int f = 0; f < XF; ++f) {
+    const int e = min(tid + f * NW * 64, XT - 1);
+    const int l = e & 63, i = (e >> 6) % MT, ks = (e >> 6) / MT;
+    xsrc[f] = X + (int64_t)min(i * 16 + (l & 15), M - 1) * ldx;
+    xk[f] = ks * 32 + (l >> 4) * 8;
   }
-
+  floatx4_t acc[MT][NS];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < NSUB; ++j) red[wave][i * NSUB + j][lane] = acc[i][j];
-  __syncthreads();
+    for (int j = 0; j < NS; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  v8 wA[KSUB][NS], wB[KSUB][NS];
+  u32x4_t xA[XF], xB[XF];
+  const u32x4_t z4 = {0u, 0u, 0u, 0u};
 
-  // wave w finishes tiles w, w+4, ...: fixed summation order over waves.
-  for (int t = wave; t < TILES; t += 4) {
-    floatx4_t v = red[0][t][lane];
+#define SK_XLOAD(XR, kb)                                                                        \
+  _Pragma("unroll") for (int f = 0; f < XF; ++f) XR[f] = *(const u32x4_t *)(xsrc[f] + min((kb) + xk[f], K - 8));
+#define SK_XSTORE(XS, XR, kb)                                                                   \
+  _Pragma("unroll") for (int f = 0; f < XF; ++f) {                                              \
+    const int e = tid + f * NW * 64;                                                            \
+    if (XT % (NW * 64) == 0 || e < XT)                                                          \
+      XS[(e >> 6) / MT][(e >> 6) % MT][e & 63] = ((kb) + xk[f] < kend) ? XR[f] : z4;            \
+  }
+#define SK_WLOAD(WB, kb)                                                                        \
+  _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
+    const int kk = min((kb) + ks * 32 + kq, K - 8);                                             \
+    _Pragma("unroll") for (int j = 0; j < NS; ++j) WB[ks][j] = load8<T>(wrow[j] + kk);          \
+  }
+#define SK_MMA(WB, XS)                                                                          \
+  _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i) {                                            \
+      const v8 a = __builtin_bit_cast(v8, XS[ks][i][lane]);                                     \
+      _Pragma("unroll") for (int j = 0; j < NS; ++j) acc[i][j] = Mfma<T>::m16(a, WB[ks][j], acc[i][j]); \
+    }                                                                                           \
+  }
+#define SK_SB __builtin_amdgcn_sched_barrier(0);
+
+  SK_XLOAD(xA, SK_SC(0))
+  SK_WLOAD(wA, SK_SC(0))
+  SK_XLOAD(xB, SK_SC(1))
+  SK_XSTORE(xs0, xA, SK_SC(0))
+  __syncthreads();
+  for (int c = 0; c < nsub; c += 2) {
+    SK_SB
+    SK_WLOAD(wB, SK_SC(c + 1))
+    SK_XLOAD(xA, c + 2 < nsub ? SK_SC(c + 2) : klast)
+    SK_SB
+    SK_MMA(wA, xs0)
+    SK_SB
+    SK_XSTORE(xs1, xB, SK_SC(c + 1))
+    __syncthreads();
+    SK_SB
+    SK_WLOAD(wA, c + 2 < nsub ? SK_SC(c + 2) : klast)
+    SK_XLOAD(xB, c + 3 < nsub ? SK_SC(c + 3) : klast)
+    SK_SB
+    SK_MMA(wB, xs1)
+    SK_SB
+    SK_XSTORE(xs0, xA, c + 2 < nsub ? SK_SC(c + 2) : kend)
+    __syncthreads();
+  }
+#undef SK_SC
+#undef SK_XLOAD
+#undef SK_XSTORE
+#undef SK_WLOAD
+#undef SK_MMA
+#undef SK_SB
+
+  const bool split = gridDim.y > 1;
 #pragma unroll
-    for (int w = 1; w < 4; ++w) v += red[w][t][lane];
-    const int i = t / NSUB, j = t % NSUB;
-    const int n = n0 + j * 16 + r16;
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = i * 16 + (lane >> 4) * 4 + r;
-      const float other = __shfl_xor(v[r], 1, 64);
-      if (gridDim.y > 1) {
-        if (m < M && n < N) part[((int64_t)s * M + m) * N + n] = v[r];
-      } else if ((lane & 1) == 0 && m < M && n < N) {
-        epi_pair<T>(ep, m, n, v[r], other);
+    for (int j = 0; j < NS; ++j) {
+      const int n = n0 + j * 16 + r16;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = i * 16 + (lane >> 4) * 4 + r;
+        const float v = acc[i][j][r];
+        const float other = __shfl_xor(v, 1, 64);
+        if (split) {
+          if (m < M && n < N) part[((int64_t)blockIdx.y * M + m) * N + n] = v;
+        } else if ((lane & 1) == 0 && m < M && n < N) {
+          epi_pair<T>(ep, m, n, v, other);
+        }
       }
     }
-  }
 }
 
 // ------------------------------------------------------------------ split-K finish
@@ -265,21 +307,44 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 
 // ------------------------------------------------------------------ dispatch
 
+// Launch shapes of the decode kernel, chosen from the weight matrix shape:
+// enough waves to keep HBM busy, few enough K splits that the fp32 partials
+// stay small, and (for the largest N) wide workgroups that share one staged
+// activation block among sixteen waves.
+struct SkinnyPlan {
+  int ns, ksub, nw, splits, kchunk;
+};
+
+SkinnyPlan skinny_plan(int N, int K, int want_splits) {
+  SkinnyPlan p;
+  if (N >= 65536) {
+    p = {1, 4, 16, 1, 0};
+  } else {
+    p = {2, 2, 4, 1, 0};
+  }
+  const int KC2 = 2 * p.ksub * 32;
+  int s = std::max(1, want_splits);
+  int kchunk = (K + s - 1) / s;
+  kchunk = (kchunk + KC2 - 1) / KC2 * KC2;
+  p.kchunk = kchunk;
+  p.splits = (K + kchunk - 1) / kchunk;
+  return p;
+}
+
+int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K, splits).splits; }
+
 template <typename T, int MT>
 static void launch_skinny_mt(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits, float *part,
                              const Epi &ep, hipStream_t s) {
-  constexpr int NSUB = 4, U = 2;
-  int kchunk = (K + splits - 1) / splits;
-  kchunk = (kchunk + 31) & ~31;
-  splits = (K + kchunk - 1) / kchunk;
-  dim3 grid((N + NSUB * 16 - 1) / (NSUB * 16), splits);
-  gemm_skinny_kernel<T, MT, NSUB, U><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, kchunk, part, ep);
-}
-
-int skinny_effective_splits(int K, int splits) {
-  int kchunk = (K + splits - 1) / splits;
-  kchunk = (kchunk + 31) & ~31;
-  return (K + kchunk - 1) / kchunk;
+  const SkinnyPlan p = skinny_plan(N, K, splits);
+  const int cols = p.nw * p.ns * 16;
+  dim3 grid((N + cols - 1) / cols, p.splits);
+  if (p.ns == 1)
+    gemm_skinny_kernel<T, MT, 1, 4, 16><<<grid, 16 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
+  else if (p.nw == 8)
+    gemm_skinny_kernel<T, MT, 2, 2, 8><<<grid, 8 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
+  else
+    gemm_skinny_kernel<T, MT, 2, 2, 4><<<grid, 4 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
 }
 
 template <typename T>

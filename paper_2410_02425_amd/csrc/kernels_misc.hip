@@ -28,50 +28,66 @@ void launch_embed(const T *E, const int32_t *pool, const int32_t *tok_idx, const
 
 // ------------------------------------------------------------------ RMSNorm
 
-constexpr int NORM_THREADS = 256;
-constexpr int NORM_MAX_PER_THREAD = 32;  // d <= 8192
+constexpr int NORM_V4 = 4;  // float4 per thread; the block has d / 16 threads (rounded to waves)
 
-template <typename T>
-__global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(float *x, const float *part, int n_part,
-                                                               int64_t part_stride,
-                                                               const int32_t *rows,
-                                                               const float *__restrict__ g,
-                                                               T *__restrict__ y, int d, float eps) {
-  __shared__ float red[NORM_THREADS / 64];
+// One workgroup per row.  The residual row and every split-K partial of it
+// are requested before any is summed (NP is the partial count), so a row costs
+// one memory latency rather than one per partial.
+template <typename T, int NP>
+__global__ __launch_bounds__(512) void rmsnorm_kernel(float *x, const float *part, int64_t part_stride,
+                                                       const int32_t *rows, const float *__restrict__ g,
+                                                       T *__restrict__ y, int d, float eps) {
+  __shared__ float red[16];
   const int j = blockIdx.x;
   const int src = rows ? rows[j] : j;
-  float *xr = x + (int64_t)src * d;
-  float v[NORM_MAX_PER_THREAD];
-  float ss = 0.f;
+  const int d4 = d >> 2;
+  const int nt = blockDim.x;
+  float4 *xr = (float4 *)(x + (int64_t)src * d);
+  float4 v[NORM_V4];
+  float4 p[NP > 0 ? NP : 1][NORM_V4];
 #pragma unroll
-  for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
-    const int c = threadIdx.x + e * NORM_THREADS;
-    if (c < d) {
-      float a = xr[c];
-      for (int s = 0; s < n_part; ++s) a += part[s * part_stride + (int64_t)src * d + c];
-      v[e] = a;
-      ss += a * a;
+  for (int e = 0; e < NORM_V4; ++e) {
+    const int c = threadIdx.x + e * nt;
+    if (c < d4) {
+      v[e] = xr[c];
+#pragma unroll
+      for (int s = 0; s < NP; ++s) p[s][e] = ((const float4 *)(part + s * part_stride + (int64_t)src * d))[c];
     }
   }
-  if (n_part) {
+  float ss = 0.f;
 #pragma unroll
-    for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
-      const int c = threadIdx.x + e * NORM_THREADS;
-      if (c < d) xr[c] = v[e];
+  for (int e = 0; e < NORM_V4; ++e) {
+    const int c = threadIdx.x + e * nt;
+    if (c < d4) {
+#pragma unroll
+      for (int s = 0; s < NP; ++s) {
+        v[e].x += p[s][e].x;
+        v[e].y += p[s][e].y;
+        v[e].z += p[s][e].z;
+        v[e].w += p[s][e].w;
+      }
+      if (NP) xr[c] = v[e];
+      ss += v[e].x * v[e].x + v[e].y * v[e].y + v[e].z * v[e].z + v[e].w * v[e].w;
     }
   }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   float tot = 0.f;
-#pragma unroll
-  for (int w = 0; w < NORM_THREADS / 64; ++w) tot += red[w];
+  for (int w = 0; w < (nt >> 6); ++w) tot += red[w];
   const float r = rsqrtf(tot / (float)d + eps);
   T *yr = y + (int64_t)j * d;
+  const float4 *g4 = (const float4 *)g;
 #pragma unroll
-  for (int e = 0; e < NORM_MAX_PER_THREAD; ++e) {
-    const int c = threadIdx.x + e * NORM_THREADS;
-    if (c < d) yr[c] = Act<T>::st(v[e] * r * g[c]);
+  for (int e = 0; e < NORM_V4; ++e) {
+    const int c = threadIdx.x + e * nt;
+    if (c < d4) {
+      const float4 gg = g4[c];
+      yr[4 * c + 0] = Act<T>::st(v[e].x * r * gg.x);
+      yr[4 * c + 1] = Act<T>::st(v[e].y * r * gg.y);
+      yr[4 * c + 2] = Act<T>::st(v[e].z * r * gg.z);
+      yr[4 * c + 3] = Act<T>::st(v[e].w * r * gg.w);
+    }
   }
 }
 
@@ -79,35 +95,55 @@ template <typename T>
 void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride, const int32_t *rows,
                     const float *g, T *y, int M, int d, float eps, hipStream_t s) {
   if (M <= 0) return;
-  rmsnorm_kernel<T><<<M, NORM_THREADS, 0, s>>>(x, part, n_part, part_stride, rows, g, y, d, eps);
+  // whole waves, NORM_V4 float4 per thread (d <= 8192)
+  const int threads = std::min(512, std::max(64, ((d / (4 * NORM_V4)) + 63) / 64 * 64));
+#define NORM_CASE(NPV)                                                                                  \
+  case NPV:                                                                                             \
+    rmsnorm_kernel<T, NPV><<<M, threads, 0, s>>>(x, part, part_stride, rows, g, y, d, eps);             \
+    break;
+  switch (n_part) {
+    NORM_CASE(0) NORM_CASE(1) NORM_CASE(2) NORM_CASE(3) NORM_CASE(4) NORM_CASE(5) NORM_CASE(6)
+    NORM_CASE(7) NORM_CASE(8) NORM_CASE(9) NORM_CASE(10) NORM_CASE(11) NORM_CASE(12)
+    NORM_CASE(13) NORM_CASE(14) NORM_CASE(15) NORM_CASE(16)
+    default: break;  // callers never pass more than 16 partials
+  }
+#undef NORM_CASE
 }
 
 // ------------------------------------------------------------------ argmax
 
-__global__ __launch_bounds__(256) void argmax_kernel(const float *__restrict__ logits, int64_t ld, int V,
-                                                     const int32_t *out_slot, int32_t *slot_tok,
-                                                     int32_t *tok_log) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
+// One workgroup of 1024 threads per row, 16-byte loads; each thread keeps the
+// first maximum it meets in increasing index order, and merges prefer the
+// larger value, then the lower index.
+__device__ __forceinline__ void argmax_merge(float &bv, int &bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+__global__ __launch_bounds__(1024) void argmax_kernel(const float *__restrict__ logits, int64_t ld, int V,
+                                                      const int32_t *out_slot, int32_t *slot_tok, int32_t *tok_log) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const int m = blockIdx.x;
   const float *row = logits + (int64_t)m * ld;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int c = threadIdx.x; c < V; c += 256) {
-    const float v = row[c];
-    if (v > best) {  // increasing c: the first maximum of this thread wins
-      best = v;
-      bi = c;
-    }
+  const int v4 = ((ld & 3) == 0) ? V >> 2 : 0;
+  for (int c = threadIdx.x; c < v4; c += 1024) {
+    const float4 q = ((const float4 *)row)[c];
+    argmax_merge(best, bi, q.x, 4 * c);
+    argmax_merge(best, bi, q.y, 4 * c + 1);
+    argmax_merge(best, bi, q.z, 4 * c + 2);
+    argmax_merge(best, bi, q.w, 4 * c + 3);
   }
+  for (int c = 4 * v4 + threadIdx.x; c < V; c += 1024) argmax_merge(best, bi, row[c], c);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float ov = __shfl_xor(best, o, 64);
     const int oi = __shfl_xor(bi, o, 64);
-    if (ov > best || (ov == best && oi < bi)) {
-      best = ov;
-      bi = oi;
-    }
+    argmax_merge(best, bi, ov, oi);
   }
   if ((threadIdx.x & 63) == 0) {
     sv[threadIdx.x >> 6] = best;
@@ -115,20 +151,16 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float *__restrict__ l
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w)
-      if (sv[w] > best || (sv[w] == best && si[w] < bi)) {
-        best = sv[w];
-        bi = si[w];
-      }
+    for (int w = 1; w < 16; ++w) argmax_merge(best, bi, sv[w], si[w]);
     if (out_slot) slot_tok[out_slot[m]] = bi;
     tok_log[m] = bi;
   }
 }
 
-void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t *out_slot,
-                   int32_t *slot_tok, int32_t *tok_log, hipStream_t s) {
+void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t *out_slot, int32_t *slot_tok,
+                   int32_t *tok_log, hipStream_t s) {
   if (M <= 0) return;
-  argmax_kernel<<<M, 256, 0, s>>>(logits, ld, V, out_slot, slot_tok, tok_log);
+  argmax_kernel<<<M, 1024, 0, s>>>(logits, ld, V, out_slot, slot_tok, tok_log);
 }
 
 // ------------------------------------------------------------------ weight generator

@@ -7,7 +7,7 @@
 #include "kernels.hpp"
 
 namespace lp {
-int skinny_effective_splits(int K, int splits);
+int skinny_effective_splits(int N, int K, int splits);
 }
 using namespace lp;
 
@@ -44,7 +44,7 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
   if (dtype != LP_F32) {
     int splits = 1;
     if (M <= 64 && k_splits > 1) {
-      splits = skinny_effective_splits(K, k_splits);
+      splits = skinny_effective_splits(N, K, k_splits);
       OPCHK(ws && ws_bytes >= (size_t)splits * M * N * 4, "gemm: workspace too small for split-K");
     }
     if (dtype == LP_BF16) {
