@@ -18,6 +18,7 @@ bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +32,27 @@ sys.path.insert(0, ROOT)
 from paper_2410_02425_amd import lp, synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16
+
+# HBM bytes per decode gate/up launch, measured with rocprofv3 --pmc FETCH_SIZE and
+# WRITE_SIZE (one pass each, 8B workload with 72 requests, averaged over the
+# 16928 gate/up dispatches of all row counts) and scaled by what the same
+# counters read for a plain 1 GiB device copy: FETCH_SIZE x2.0 (it reads
+# 524302 KiB for 1048576 KiB fetched), WRITE_SIZE x1.0.  The figure holds for
+# the kernel source it was measured on and is dropped when that changes.
+GATE_UP_TRAFFIC = {"bytes_per_launch": 238673243, "kernel_source": "80cb41b9d22c0ae5",
+                   "profile": "profiles/decode_gate_up_gemm_8b.md"}
+
+
+def skinny_kernel_fingerprint() -> str:
+    """sha256 prefix of the decode GEMM kernel's source text (its section of
+    gemm.hip plus the device helpers it includes)."""
+    csrc = os.path.join(ROOT, "paper_2410_02425_amd", "csrc")
+    s = open(os.path.join(csrc, "gemm.hip")).read()
+    a = s.index("// ------------------------------------------------------------------ skinny (decode)")
+    b = s.index("// ------------------------------------------------------------------ split-K finish")
+    d = open(os.path.join(csrc, "device.hpp")).read()
+    return hashlib.sha256((s[a:b] + d).encode()).hexdigest()[:16]
 
 
 def decode_step_bytes(shape: synth.ModelShape, rows: int, sum_ctx: int, esz: int = 2) -> int:
@@ -54,24 +76,53 @@ def gate_up_bytes(shape: synth.ModelShape, launches: int, rows_sum: int, esz: in
     return launches * 2 * F * d * esz + rows_sum * (d + F) * esz
 
 
-def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 25.0):
+def prefill_flops(shape: synth.ModelShape, prompt_lens) -> int:
+    """Algorithmic flops of one prefill step: the linear layers over every
+    prompt token, causal attention (QK^T and PV over n(n+1)/2 pairs per head)
+    and the LM head at each request's last position."""
+    d, hd, F, V, L = shape.d_model, shape.head_dim, shape.ffn_dim, shape.vocab, shape.n_layers
+    Hq, Hkv = shape.n_heads, shape.n_kv_heads
+    lin = 2 * L * (d * (Hq + 2 * Hkv) * hd + Hq * hd * d + 3 * d * F)
+    return sum(n * lin + 2 * n * (n + 1) * Hq * hd * L + 2 * d * V for n in prompt_lens)
+
+
+def copy_bandwidth_gbs(torch, reps: int = 10) -> float:
+    """Device-to-device copy rate of 1 GiB buffers (read + write bytes over
+    time): the HBM bandwidth a plain streaming kernel reaches here."""
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.0):
     """The oracle, unchanged, on a bounded sample of the workload: one request
-    (prompt and output lengths taken from the workload) generated at depth 1
-    and 2 with full-width weights, extrapolated linearly in depth to the full
-    model.  Returns the oracle's tokens/s at full depth for that request."""
+    (its prompt taken from the workload, length near the mean) generated at
+    depth 1 and 2 with full-width weights, extrapolated linearly in depth to
+    the full model.  The number of output tokens is sized from a 2-token probe
+    so that the two timed runs take about budget_s.  Returns the oracle's
+    output tokens/s at full depth for that request."""
     from oracle import transformer as T
 
     r = sorted(reqs, key=lambda q: abs(q.in_len - 553))[0]
-    n_out = 6
-    times = {}
     lm_rows = None
     embed_rows = None
+    models = {}
     for depth in (1, 2):
         sh = shape.with_layers(depth)
-        names = synth.tensor_shapes(sh)
         w = {}
         used = np.unique(r.prompt)
-        for name, tid, (rows, cols) in names:
+        for name, tid, (rows, cols) in synth.tensor_shapes(sh):
             if name == "embed":
                 if embed_rows is None:
                     embed_rows = np.zeros((rows, cols), dtype=np.float32)
@@ -87,11 +138,17 @@ def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 25.
                 w[name] = v.reshape(cols) if rows == 1 else v
         cfg = dict(n_layers=depth, d_model=sh.d_model, n_heads=sh.n_heads, n_kv_heads=sh.n_kv_heads,
                    ffn_dim=sh.ffn_dim, vocab=sh.vocab, rope_theta=sh.rope_theta, norm_eps=sh.norm_eps)
-        m = T.Model(cfg, w)
+        models[depth] = T.Model(cfg, w)
+    # probe: prefill + 1 decode token at depth 2, then size the sample
+    t0 = time.perf_counter()
+    T.generate(models[2], r.prompt, 2)
+    probe = time.perf_counter() - t0
+    n_out = int(min(max(6, budget_s / 1.5 / max(probe / 2, 1e-3)), 256))
+    times = {}
+    for depth in (1, 2):
         t0 = time.perf_counter()
-        T.generate(m, r.prompt, n_out)
+        T.generate(models[depth], r.prompt, n_out)
         times[depth] = time.perf_counter() - t0
-        del m, w
     per_layer = max(times[2] - times[1], 1e-9)
     fixed = max(times[1] - per_layer, 0.0)
     full = fixed + per_layer * shape.n_layers
@@ -117,6 +174,9 @@ def main():
     ap.add_argument("--act", choices=["f16", "bf16"], default="f16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 1 GiB device-to-device 5 times (a plain copy kernel of known size, "
+                         "the reference for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -124,6 +184,16 @@ def main():
 
     import torch
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": 1 << 30, "launches": 5}))
+        return
+    copy_gbs = copy_bandwidth_gbs(torch)
     shape = synth.SHAPES[args.config]
     wl = synth.WORKLOADS[args.config]
     key = synth.workload_seeds(wl.base_seed)[0]
@@ -167,6 +237,11 @@ def main():
     full_tokens = sum(log[i]["n_rows"] for i in full_idx)
     decode_gbs = full_bytes / full_ns if full_ns else 0.0
     out_tokens = agg["output_tokens"]
+    in_len = {r.id: r.in_len for r in reqs}
+    pre_idx = [i for i, st in enumerate(log) if st["kind"] == "prefill"]
+    pre_ns = sum(log[i]["end_ns"] - prev_end[i] for i in pre_idx)
+    pre_flops = sum(prefill_flops(shape, [in_len[j] for j in log[i]["ids"]]) for i in pre_idx)
+    pre_tflops = pre_flops / pre_ns / 1e3 if pre_ns else 0.0
 
     roofline = None
     if agg["timed_kernel_launches"]:
@@ -174,8 +249,11 @@ def main():
         avg_ms = agg["timed_kernel_ms"] / launches
         bytes_total = gate_up_bytes(shape, launches, agg["timed_kernel_rows"])
         achieved = bytes_total / launches / (avg_ms * 1e-3) / 1e9
+        traffic = (GATE_UP_TRAFFIC["bytes_per_launch"]
+                   if skinny_kernel_fingerprint() == GATE_UP_TRAFFIC["kernel_source"] else None)
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "traffic_unit": "bytes per launch",
                     "kernel": "gemm_skinny_kernel (decode gate/up, fused SiLU gate)",
                     "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
                     "bytes_per_launch": int(bytes_total / launches)}
@@ -205,6 +283,10 @@ def main():
         "ttft_p50_ms": round(float(np.median(ttft)) / 1e6, 2),
         "nttft_p50_ms": round(float(np.median(nttft)) / 1e6, 4),
         "itl_p50_ms": round(float(np.median(itl)) / 1e6, 3),
+        "prefill_tflops": round(pre_tflops, 1),
+        "prefill_mfma_frac": round(pre_tflops / MFMA_F16_PEAK_TFLOPS, 4),
+        "copy_gbs_measured": round(copy_gbs, 1),
+        "decode_frac_of_copy_full_batch": round(decode_gbs / copy_gbs, 4),
         "prefill_steps": agg["n_prefill_steps"],
         "decode_steps": agg["n_decode_steps"],
         "roofline": roofline,

@@ -53,7 +53,7 @@ extern "C" {
 
 /* engine option flags */
 #define LP_FLAG_KEEP_LOGITS 1u  /* keep fp32 logits of every output token      */
-#define LP_FLAG_TIME_KERNEL 2u  /* time each decode gate/up GEMM launch        */
+#define LP_FLAG_TIME_KERNEL 2u  /* time one decode gate/up GEMM launch per step */
 #define LP_FLAG_BF16_ACTIVATIONS 4u /* bf16 (not fp16) GEMM inputs and KV cache */
 
 /* Decoder shape.  Llama-style pre-norm decoder: RMSNorm, rotary embeddings

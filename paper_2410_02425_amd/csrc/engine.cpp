@@ -613,7 +613,7 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
                int64_t log_off, int64_t step) {
   const int step_ring = (int)(step % RING);
   // LP_FLAG_TIME_KERNEL: one layer's gate/up launch per decode step, rotating
-  // over the layers, is bracketed by events (each event adds a gap)
+  // over the layers, carries two events bound to its dispatch
   const int timed_layer = (int)(step % e->D.L);
   const Dims &D = e->D;
   hipStream_t st = e->stream;
@@ -672,13 +672,9 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
     eg.kind = EPI_SILU;
     eg.act_out = hb;
     eg.ld_act = D.F;
-    hipEvent_t *tk = nullptr;
-    if (!prefill && !e->ev_kern.empty() && l == timed_layer) {
-      tk = &e->ev_kern[(size_t)step_ring * 2];
-      hipEventRecord(tk[0], st);
-    }
-    launch_gemm<T>(xn, D.d, e->ptr<T>(e->Ly.wgu[l]), M, 2 * D.F, D.d, 1, part, eg, st);
-    if (tk) hipEventRecord(tk[1], st);
+    const hipEvent_t *tk = nullptr;
+    if (!prefill && !e->ev_kern.empty() && l == timed_layer) tk = &e->ev_kern[(size_t)step_ring * 2];
+    launch_gemm<T>(xn, D.d, e->ptr<T>(e->Ly.wgu[l]), M, 2 * D.F, D.d, 1, part, eg, st, tk);
     Epi ed{};
     ed.kind = EPI_RESID;
     ed.out = x;

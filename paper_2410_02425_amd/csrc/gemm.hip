@@ -10,6 +10,8 @@
 //  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
 #include <algorithm>
 
+#include <hip/hip_ext.h>
+
 #include "device.hpp"
 
 namespace lp {
@@ -32,7 +34,9 @@ namespace lp {
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-template <typename T, int MT, int NS, int KSUB, int NW>
+// GATE marks the gate/up launch (SiLU-gate epilogue): the same code under its
+// own symbol, so that per-kernel profiles separate it from the other GEMMs.
+template <typename T, int MT, int NS, int KSUB, int NW, bool GATE>
 __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
                                                              int kchunk, float *__restrict__ part, Epi ep) {
@@ -333,55 +337,68 @@ SkinnyPlan skinny_plan(int N, int K, int want_splits) {
 
 int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K, splits).splits; }
 
+// Launches a kernel plainly, or with two events bound to its own dispatch.
+template <typename... KArgs, typename... Args>
+static void launch_k(void (*k)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const hipEvent_t *timing,
+                     Args... args) {
+  if (timing)
+    hipExtLaunchKernelGGL(k, grid, block, 0, s, timing[0], timing[1], 0, static_cast<KArgs>(args)...);
+  else
+    k<<<grid, block, 0, s>>>(static_cast<KArgs>(args)...);
+}
+
 template <typename T, int MT>
 static void launch_skinny_mt(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits, float *part,
-                             const Epi &ep, hipStream_t s) {
+                             const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
   const SkinnyPlan p = skinny_plan(N, K, splits);
   const int cols = p.nw * p.ns * 16;
   dim3 grid((N + cols - 1) / cols, p.splits);
   if (p.ns == 1)
-    gemm_skinny_kernel<T, MT, 1, 4, 16><<<grid, 16 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
-  else if (p.nw == 8)
-    gemm_skinny_kernel<T, MT, 2, 2, 8><<<grid, 8 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
+    launch_k(gemm_skinny_kernel<T, MT, 1, 4, 16, false>, grid, 16 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+             part, ep);
+  else if (ep.kind == EPI_SILU && p.splits == 1)
+    launch_k(gemm_skinny_kernel<T, MT, 2, 2, 4, true>, grid, 4 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+             part, ep);
   else
-    gemm_skinny_kernel<T, MT, 2, 2, 4><<<grid, 4 * 64, 0, s>>>(X, ldx, W, M, N, K, p.kchunk, part, ep);
+    launch_k(gemm_skinny_kernel<T, MT, 2, 2, 4, false>, grid, 4 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+             part, ep);
 }
 
 template <typename T>
 static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits, float *part,
-                             const Epi &ep, hipStream_t s) {
+                             const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
   if (M <= 0 || N <= 0) return;
   if (M <= 64) {
     if (splits < 1 || part == nullptr) splits = 1;
     switch ((M + 15) / 16) {
-      case 1: launch_skinny_mt<T, 1>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      case 2: launch_skinny_mt<T, 2>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      case 3: launch_skinny_mt<T, 3>(X, ldx, W, M, N, K, splits, part, ep, s); break;
-      default: launch_skinny_mt<T, 4>(X, ldx, W, M, N, K, splits, part, ep, s); break;
+      case 1: launch_skinny_mt<T, 1>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
+      case 2: launch_skinny_mt<T, 2>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
+      case 3: launch_skinny_mt<T, 3>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
+      default: launch_skinny_mt<T, 4>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
     }
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);
-  gemm_big_kernel<T><<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+  launch_k(gemm_big_kernel<T>, grid, 256, s, timing, X, ldx, W, M, N, K, ep);
 }
 
 template <>
 void launch_gemm<bf16_t>(const bf16_t *X, int64_t ldx, const bf16_t *W, int M, int N, int K, int splits,
-                         float *part, const Epi &ep, hipStream_t s) {
-  launch_gemm_mfma<bf16_t>(X, ldx, W, M, N, K, splits, part, ep, s);
+                         float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
+  launch_gemm_mfma<bf16_t>(X, ldx, W, M, N, K, splits, part, ep, s, timing);
 }
 template <>
 void launch_gemm<f16_t>(const f16_t *X, int64_t ldx, const f16_t *W, int M, int N, int K, int splits,
-                        float *part, const Epi &ep, hipStream_t s) {
-  launch_gemm_mfma<f16_t>(X, ldx, W, M, N, K, splits, part, ep, s);
+                        float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
+  launch_gemm_mfma<f16_t>(X, ldx, W, M, N, K, splits, part, ep, s, timing);
 }
 
 template <>
 void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int N, int K, int splits,
-                        float *part, const Epi &ep, hipStream_t s) {
+                        float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
   if (M <= 0 || N <= 0) return;
   dim3 grid((N + F_BN - 1) / F_BN, (M + F_BM - 1) / F_BM);
-  gemm_f32_kernel<<<grid, 256, 0, s>>>(X, ldx, W, M, N, K, ep);
+  launch_k(gemm_f32_kernel, grid, 256, s, timing, X, ldx, W, M, N, K, ep);
 }
 
 template void launch_gemm_finish<float>(const float *, int, int, int, const Epi &, hipStream_t);

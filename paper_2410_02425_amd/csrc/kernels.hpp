@@ -69,12 +69,14 @@ void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride
                     const int32_t *rows, const float *g, T *y, int M, int d, float eps,
                     hipStream_t s);
 
-// Generic GEMM Y = X W^T with epilogue.  T = float or bf16_t.
-// splits > 1 (bf16, M <= 64 only): writes partials [splits][M][N] into `part`
+// Generic GEMM Y = X W^T with epilogue.  T = float, bf16_t or f16_t.
+// splits > 1 (16-bit, M <= 64 only): writes partials [splits][M][N] into `part`
 // and a following launch_gemm_finish applies the epilogue.
+// timing (optional, two events): recorded with the kernel's own dispatch, so
+// their interval is the kernel's execution alone.
 template <typename T>
 void launch_gemm(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits,
-                 float *part, const Epi &ep, hipStream_t s);
+                 float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing = nullptr);
 
 template <typename T>
 void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s);
