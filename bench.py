@@ -139,11 +139,15 @@ def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.
         cfg = dict(n_layers=depth, d_model=sh.d_model, n_heads=sh.n_heads, n_kv_heads=sh.n_kv_heads,
                    ffn_dim=sh.ffn_dim, vocab=sh.vocab, rope_theta=sh.rope_theta, norm_eps=sh.norm_eps)
         models[depth] = T.Model(cfg, w)
-    # probe: prefill + 1 decode token at depth 2, then size the sample
+    # probes at depth 2: prefill alone (1 token) and prefill + 3 decode tokens;
+    # size the sample so that both timed runs together take about budget_s
     t0 = time.perf_counter()
-    T.generate(models[2], r.prompt, 2)
-    probe = time.perf_counter() - t0
-    n_out = int(min(max(6, budget_s / 1.5 / max(probe / 2, 1e-3)), 256))
+    T.generate(models[2], r.prompt, 1)
+    t_pre = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    T.generate(models[2], r.prompt, 4)
+    per_tok = max((time.perf_counter() - t0 - t_pre) / 3, 1e-4)
+    n_out = int(min(max(6, (budget_s - 2 * t_pre) / (1.75 * per_tok)), 1024))
     times = {}
     for depth in (1, 2):
         t0 = time.perf_counter()

@@ -23,10 +23,11 @@ extern "C" {
 
 /* Y[M x N] (fp32, row stride N) = X[M x K] (row stride ldx) times W[N x K]^T:
  * the weight-GEMM contraction of every projection of the decoder (Q/K/V,
- * output, gate/up, down, LM head).  bf16 with M <= 64 takes the decode
- * kernel; `k_splits` > 1 splits K across workgroups and needs `ws` of at
- * least k_splits * M * N * 4 bytes (fp32 partials).  Larger M takes the
- * prefill kernel.  K must be a multiple of 8, N even; 16-byte aligned rows. */
+ * output, gate/up, down, LM head).  16-bit types with M <= 64 take the
+ * decode kernel, larger M the prefill kernel; `k_splits` > 1 splits K across
+ * workgroups (prefill: only when K is a multiple of 128; the count is rounded
+ * to whole K chunks) and needs `ws` of at least k_splits * M * N * 4 bytes
+ * (fp32 partials).  K must be a multiple of 8, N even; 16-byte aligned rows. */
 int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
                int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *hip_stream);
 

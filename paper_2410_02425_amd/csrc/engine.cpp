@@ -16,9 +16,6 @@
 #include "kernels.hpp"
 #include "scheduler.hpp"
 
-namespace lp {
-int skinny_effective_splits(int N, int K, int splits);
-}
 
 using namespace lp;
 
@@ -82,16 +79,28 @@ int decode_splits(int N, int K) {
   const int waves_per_split = std::max(1, N / 32);
   int s = std::max(1, (1024 + waves_per_split - 1) / waves_per_split);
   s = std::min(s, std::max(1, K / 512));
-  return lp::skinny_effective_splits(N, K, s);
+  return lp::gemm_effective_splits(64, N, K, s);
 }
 
-size_t part_bytes_for(const Dims &D, const lp_model_config &c, int max_batch) {
+// K splits of a GEMM over M rows whose epilogue can be deferred to a folding
+// pass: decode-sized M by the weight shape, prefill-sized M by the tile grid.
+int step_splits(int M, int N, int K) { return M <= 64 ? decode_splits(N, K) : lp::prefill_gemm_splits(M, N, K); }
+
+size_t part_bytes_for(const Dims &D, const lp_model_config &c, const lp_engine_options &o) {
   if (c.dtype != LP_BF16) return 256;
   size_t m = 0;
   const int64_t Ns[3] = {D.qkv_n, D.d, D.d};
   const int64_t Ks[3] = {D.d, D.Hq * D.hd, D.F};
-  for (int i = 0; i < 3; ++i)
-    m = std::max(m, (size_t)decode_splits((int)Ns[i], (int)Ks[i]) * max_batch * Ns[i] * sizeof(float));
+  const int64_t R = rows_cap(o);
+  for (int i = 0; i < 3; ++i) {
+    // the split count changes only where the row-tile count does: check each
+    // tile boundary (and R itself) up to the largest step
+    for (int64_t M = std::min<int64_t>(R, o.max_batch); M <= R;) {
+      m = std::max(m, (size_t)step_splits((int)M, (int)Ns[i], (int)Ks[i]) * M * Ns[i] * sizeof(float));
+      if (M == R) break;
+      M = std::min<int64_t>(R, std::max<int64_t>(M + 1, (M / 256 + 1) * 256));
+    }
+  }
   return m;
 }
 
@@ -125,7 +134,7 @@ Layout plan_layout(const lp_model_config &c, const lp_engine_options &o, int64_t
   Ly.attn = take((size_t)R * D.Hq * D.hd * D.esz);
   Ly.h = take((size_t)R * D.F * D.esz);
   Ly.logits = take((size_t)o.max_batch * D.V * 4);
-  Ly.part_bytes = part_bytes_for(D, c, o.max_batch);
+  Ly.part_bytes = part_bytes_for(D, c, o);
   Ly.part = take(Ly.part_bytes);
   Ly.attn_ws = take(decode_attention_ws_bytes(o.max_batch, D.Hq, D.hd, max_pos));
   Ly.rope_cos = take((size_t)max_pos * (D.hd / 2) * 4);
@@ -628,11 +637,10 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
   RowMeta rows{dm.row_slot, dm.row_pos};
   KVCache kv = kv_of<T>(e, dm.block_table);
   const int qd = D.Hq * D.hd;
-  // decode split-K plan (bf16 only)
-  const bool split = bf && !prefill;
-  const int s_qkv = split ? decode_splits(D.qkv_n, D.d) : 1;
-  const int s_o = split ? decode_splits(D.d, qd) : 1;
-  const int s_dn = split ? decode_splits(D.d, D.F) : 1;
+  // split-K plan (16-bit paths only)
+  const int s_qkv = bf ? step_splits(M, D.qkv_n, D.d) : 1;
+  const int s_o = bf ? step_splits(M, D.d, qd) : 1;
+  const int s_dn = bf ? step_splits(M, D.d, D.F) : 1;
   int pending_parts = 0;  // partials of the last residual GEMM not yet folded into x
   int64_t pending_stride = 0;
   for (int l = 0; l < D.L; ++l) {

@@ -258,6 +258,157 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
     }
 }
 
+// ------------------------------------------------------------------ prefill (M > 64)
+//
+// 256x256 output tiles, eight waves (4 x 2, each 64 x 128 = 2 x 4 MFMA 32x32x16
+// tiles), 64-wide K stages.  Global loads run two stages ahead of the MFMAs
+// in two register sets, so each load has two stages of MFMA work to land in;
+// the staged tile goes to one of two LDS buffers.  LDS rows are 128 bytes
+// (one K stage) with the sixteen-byte chunks XOR-swizzled by row, so that the
+// coalesced row stores and the 32-row MFMA fragment reads are both free of
+// bank conflicts.  gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the
+// epilogue.  Rows and columns past M / N read clamped (valid) memory and are
+// never stored; K must be a multiple of 128 (an even number of stages per
+// split).
+
+constexpr int PF_BM = 256, PF_BN = 256, PF_BK = 64, PF_WM = 4, PF_WN = 2, PF_NT = PF_WM * PF_WN * 64;
+constexpr int PF_STAGE = (PF_BM + PF_BN) * PF_BK;  // elements per LDS buffer
+
+__device__ __forceinline__ int pf_swz(int row, int c) { return row * PF_BK + ((c ^ (row & 7)) << 3); }
+
+template <typename T>
+__global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
+                                                             const T *__restrict__ W, int M, int N, int K,
+                                                             int kchunk, float *__restrict__ part, Epi ep) {
+  typedef typename Mfma<T>::v8 v8;
+  constexpr int TM = PF_BM / PF_WM / 32, TN = PF_BN / PF_WN / 32;  // MFMA tiles per wave
+  constexpr int CA = PF_BM * 8 / PF_NT, CB = PF_BN * 8 / PF_NT;   // 16-byte chunks per thread
+  __shared__ __attribute__((aligned(16))) T lds[2 * PF_STAGE];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / PF_WN, wn = wave % PF_WN;
+  const int m0 = blockIdx.y * PF_BM, n0 = blockIdx.x * PF_BN;
+  const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
+  const int nk = (ke - kb) / PF_BK;
+
+  const T *ga[CA];
+  const T *gb[CB];
+  int la[CA], lb[CB];
+#pragma unroll
+  for (int i = 0; i < CA; ++i) {
+    const int idx = tid + i * PF_NT, row = idx >> 3, c = idx & 7;
+    ga[i] = X + (int64_t)min(m0 + row, M - 1) * ldx + kb + c * 8;
+    la[i] = pf_swz(row, c);
+  }
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    const int idx = tid + i * PF_NT, row = idx >> 3, c = idx & 7;
+    gb[i] = W + (int64_t)min(n0 + row, N - 1) * K + kb + c * 8;
+    lb[i] = PF_BM * PF_BK + pf_swz(row, c);
+  }
+  u32x4_t r0a[CA], r0b[CB], r1a[CA], r1b[CB];
+  floatx16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  int fa[TM], fb[TN];  // LDS rows of this lane's fragments
+#pragma unroll
+  for (int i = 0; i < TM; ++i) fa[i] = wm * (PF_BM / PF_WM) + i * 32 + (lane & 31);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) fb[j] = wn * (PF_BN / PF_WN) + j * 32 + (lane & 31);
+  const int kh = lane >> 5;
+
+#define PF_LOAD(RA, RB, kt)                                                                        \
+  _Pragma("unroll") for (int i = 0; i < CA; ++i) RA[i] = *(const u32x4_t *)(ga[i] + (kt) * PF_BK); \
+  _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = *(const u32x4_t *)(gb[i] + (kt) * PF_BK);
+#define PF_STORE(RA, RB, buf)                                                                      \
+  _Pragma("unroll") for (int i = 0; i < CA; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + la[i]) = RA[i]; \
+  _Pragma("unroll") for (int i = 0; i < CB; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + lb[i]) = RB[i];
+#define PF_MMA(buf)                                                                                \
+  _Pragma("unroll") for (int ks = 0; ks < PF_BK / 16; ++ks) {                                      \
+    v8 a[TM], b[TN];                                                                               \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                 \
+      a[i] = load8<T>(lds + (buf) * PF_STAGE + pf_swz(fa[i], ks * 2 + kh));                        \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                 \
+      b[j] = load8<T>(lds + (buf) * PF_STAGE + PF_BM * PF_BK + pf_swz(fb[j], ks * 2 + kh));        \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                 \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::m32(a[i], b[j], acc[i][j]); \
+  }
+
+  // stage s is loaded into register set s % 2 two stages before its MFMAs
+  PF_LOAD(r0a, r0b, 0)
+  PF_LOAD(r1a, r1b, min(1, nk - 1))
+  PF_STORE(r0a, r0b, 0)
+  PF_LOAD(r0a, r0b, min(2, nk - 1))
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    PF_MMA(0)
+    PF_STORE(r1a, r1b, 1)
+    PF_LOAD(r1a, r1b, min(kt + 3, nk - 1))
+    __syncthreads();
+    PF_MMA(1)
+    PF_STORE(r0a, r0b, 0)
+    PF_LOAD(r0a, r0b, min(kt + 4, nk - 1))
+    __syncthreads();
+  }
+#undef PF_LOAD
+#undef PF_STORE
+#undef PF_MMA
+
+  // accumulator (i, j, r) of lane l: row (r & 3) + 4 (l / 32) + 8 (r / 4), column l % 32
+  const int wrow = m0 + wm * (PF_BM / PF_WM), wcol = n0 + wn * (PF_BN / PF_WN);
+  if (gridDim.z > 1) {
+    float *pz = part + (int64_t)blockIdx.z * M * N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = wcol + j * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = wrow + i * 32 + (r & 3) + 4 * (lane >> 5) + 8 * (r >> 2);
+          if (m < M && n < N) pz[(int64_t)m * N + n] = acc[i][j][r];
+        }
+      }
+    return;
+  }
+  // epilogue through LDS (free after the last stage): each wave stages 32 rows
+  // x 128 columns of fp32 at a time in its own 16 KB, then its lanes apply the
+  // epilogue to column pairs, one 128-column row per pass of the wave
+  constexpr int SROW = PF_BN / PF_WN;  // fp32 row stride of the staging tile
+  static_assert(PF_WM * PF_WN * 32 * SROW * 4 <= 2 * PF_STAGE * (int)sizeof(T), "staging fits in LDS");
+  float *stg = (float *)lds + wave * 32 * SROW;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        stg[((r & 3) + 4 * (lane >> 5) + 8 * (r >> 2)) * SROW + j * 32 + (lane & 31)] = acc[i][j][r];
+    __syncthreads();
+    for (int row = 0; row < 32; ++row) {
+      const int m = wrow + i * 32 + row, n = wcol + lane * 2;
+      const float2 v = *(const float2 *)(stg + row * SROW + lane * 2);
+      if (m < M && n < N) epi_pair<T>(ep, m, n, v.x, v.y);
+    }
+    __syncthreads();
+  }
+}
+
+// K splits of a prefill GEMM: only when the tile grid alone leaves most of the
+// chip idle (the fp32 partials cost HBM traffic), and never below 1024 k per
+// split.  Returns the count the launch will use.
+int prefill_gemm_splits(int M, int N, int K) {
+  if (M <= 64 || K % (2 * PF_BK) != 0) return 1;
+  const int64_t tiles = (int64_t)((M + PF_BM - 1) / PF_BM) * ((N + PF_BN - 1) / PF_BN);
+  int s = tiles < 64 ? 4 : tiles < 160 ? 2 : 1;
+  s = std::max(1, std::min(s, K / 1024));
+  const int kchunk = (K / s + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+  return (K + kchunk - 1) / kchunk;
+}
+
 // ------------------------------------------------------------------ fp32 path
 
 constexpr int F_BM = 64, F_BN = 64, F_BK = 16;
@@ -337,6 +488,14 @@ SkinnyPlan skinny_plan(int N, int K, int want_splits) {
 
 int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K, splits).splits; }
 
+int gemm_effective_splits(int M, int N, int K, int splits) {
+  if (splits <= 1) return 1;
+  if (M <= 64) return skinny_effective_splits(N, K, splits);
+  if (K % (2 * PF_BK) != 0) return 1;
+  const int kchunk = (K / splits + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+  return (K + kchunk - 1) / kchunk;
+}
+
 // Launches a kernel plainly, or with two events bound to its own dispatch.
 template <typename... KArgs, typename... Args>
 static void launch_k(void (*k)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const hipEvent_t *timing,
@@ -376,6 +535,14 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
       case 3: launch_skinny_mt<T, 3>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
       default: launch_skinny_mt<T, 4>(X, ldx, W, M, N, K, splits, part, ep, s, timing); break;
     }
+    return;
+  }
+  if (K % (2 * PF_BK) == 0) {
+    if (splits < 1 || part == nullptr) splits = 1;
+    int kchunk = (K / splits + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+    const int z = (K + kchunk - 1) / kchunk;
+    dim3 grid((N + PF_BN - 1) / PF_BN, (M + PF_BM - 1) / PF_BM, z);
+    launch_k(gemm_prefill_kernel<T>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);

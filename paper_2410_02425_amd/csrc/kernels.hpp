@@ -70,13 +70,19 @@ void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride
                     hipStream_t s);
 
 // Generic GEMM Y = X W^T with epilogue.  T = float, bf16_t or f16_t.
-// splits > 1 (16-bit, M <= 64 only): writes partials [splits][M][N] into `part`
-// and a following launch_gemm_finish applies the epilogue.
+// splits > 1 (16-bit only): writes partials [splits][M][N] into `part` and a
+// following launch_gemm_finish (or an RMSNorm fold) applies the epilogue;
+// gemm_effective_splits gives the count a launch uses for a requested one.
 // timing (optional, two events): recorded with the kernel's own dispatch, so
 // their interval is the kernel's execution alone.
 template <typename T>
 void launch_gemm(const T *X, int64_t ldx, const T *W, int M, int N, int K, int splits,
                  float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing = nullptr);
+
+int gemm_effective_splits(int M, int N, int K, int splits);
+// K splits the prefill GEMM (M > 64) takes for its shape (1 when the tile grid
+// fills the chip); an effective count.
+int prefill_gemm_splits(int M, int N, int K);
 
 template <typename T>
 void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s);

@@ -6,9 +6,6 @@
 #include "../../include/lp_ops.h"
 #include "kernels.hpp"
 
-namespace lp {
-int skinny_effective_splits(int N, int K, int splits);
-}
 using namespace lp;
 
 std::string &lp_global_error();
@@ -43,9 +40,9 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
   ep.ldo = N;
   if (dtype != LP_F32) {
     int splits = 1;
-    if (M <= 64 && k_splits > 1) {
-      splits = skinny_effective_splits(N, K, k_splits);
-      OPCHK(ws && ws_bytes >= (size_t)splits * M * N * 4, "gemm: workspace too small for split-K");
+    if (k_splits > 1) {
+      splits = gemm_effective_splits(M, N, K, k_splits);
+      OPCHK(splits == 1 || (ws && ws_bytes >= (size_t)splits * M * N * 4), "gemm: workspace too small for split-K");
     }
     if (dtype == LP_BF16) {
       launch_gemm<bf16_t>((const bf16_t *)X, ldx, (const bf16_t *)W, M, N, K, splits, (float *)ws, ep, s);

@@ -34,8 +34,10 @@ GEMM_CASES = [
     # M, N, K, splits -- decode kernel (M <= 64) with and without split-K, tails in M, N and K
     (1, 96, 256, 1), (16, 768, 256, 1), (37, 1376, 688, 3), (64, 1024, 256, 2),
     (64, 6144, 4096, 6), (64, 4096, 14336, 8), (5, 2000, 1000, 4),
-    # prefill kernel
-    (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1),
+    # prefill kernels: K not a multiple of 128 (LDS-tiled fallback), then the
+    # pipelined kernel with tails in M and N, split-K, long K
+    (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1), (300, 640, 4096, 4),
+    (513, 1000, 1024, 2), (777, 6144, 4096, 1), (600, 1536, 14336, 4), (1030, 512, 384, 3),
 ]
 
 
