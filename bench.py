@@ -45,14 +45,16 @@ GATE_UP_TRAFFIC = {"bytes_per_launch": 238673243, "kernel_source": "80cb41b9d22c
 
 
 def skinny_kernel_fingerprint() -> str:
-    """sha256 prefix of the decode GEMM kernel's source text (its section of
-    gemm.hip plus the device helpers it includes)."""
+    """sha256 prefix of the decode GEMM kernel's source text: its section of
+    gemm.hip, its launch plan, and the device helpers it includes."""
     csrc = os.path.join(ROOT, "paper_2410_02425_amd", "csrc")
     s = open(os.path.join(csrc, "gemm.hip")).read()
     a = s.index("// ------------------------------------------------------------------ skinny (decode)")
     b = s.index("// ------------------------------------------------------------------ split-K finish")
+    c = s.index("struct SkinnyPlan {")
+    e = s.index("static void launch_gemm_mfma(")
     d = open(os.path.join(csrc, "device.hpp")).read()
-    return hashlib.sha256((s[a:b] + d).encode()).hexdigest()[:16]
+    return hashlib.sha256((s[a:b] + s[c:e] + d).encode()).hexdigest()[:16]
 
 
 def decode_step_bytes(shape: synth.ModelShape, rows: int, sum_ctx: int, esz: int = 2) -> int:

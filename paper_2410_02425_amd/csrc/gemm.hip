@@ -463,9 +463,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 // ------------------------------------------------------------------ dispatch
 
 // Launch shapes of the decode kernel, chosen from the weight matrix shape:
-// enough waves to keep HBM busy, few enough K splits that the fp32 partials
-// stay small, and (for the largest N) wide workgroups that share one staged
-// activation block among sixteen waves.
+// one 16-column slice per wave, eight waves per workgroup sharing the staged
+// activations, and (for the largest N) sixteen waves with deeper sub-chunks.
 struct SkinnyPlan {
   int ns, ksub, nw, splits, kchunk;
 };
@@ -475,7 +474,7 @@ SkinnyPlan skinny_plan(int N, int K, int want_splits) {
   if (N >= 65536) {
     p = {1, 4, 16, 1, 0};
   } else {
-    p = {2, 2, 4, 1, 0};
+    p = {1, 2, 8, 1, 0};
   }
   const int KC2 = 2 * p.ksub * 32;
   int s = std::max(1, want_splits);
@@ -512,14 +511,14 @@ static void launch_skinny_mt(const T *X, int64_t ldx, const T *W, int M, int N, 
   const SkinnyPlan p = skinny_plan(N, K, splits);
   const int cols = p.nw * p.ns * 16;
   dim3 grid((N + cols - 1) / cols, p.splits);
-  if (p.ns == 1)
+  if (p.nw == 16)
     launch_k(gemm_skinny_kernel<T, MT, 1, 4, 16, false>, grid, 16 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
              part, ep);
   else if (ep.kind == EPI_SILU && p.splits == 1)
-    launch_k(gemm_skinny_kernel<T, MT, 2, 2, 4, true>, grid, 4 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+    launch_k(gemm_skinny_kernel<T, MT, 1, 2, 8, true>, grid, 8 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
              part, ep);
   else
-    launch_k(gemm_skinny_kernel<T, MT, 2, 2, 4, false>, grid, 4 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+    launch_k(gemm_skinny_kernel<T, MT, 1, 2, 8, false>, grid, 8 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
              part, ep);
 }
 
