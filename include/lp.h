@@ -197,6 +197,28 @@ int lp_sched_simulate(const lp_request *reqs, int32_t n, int32_t max_batch,
                       int64_t *row_ids, int32_t *row_slots, int64_t row_cap, int64_t *token_ns,
                       int64_t tok_cap, int64_t *arrival_ns);
 
+/* Load-test metrics (Sec. III-C-3) of one experiment: n requests with their
+ * arrival times, input and output lengths, and the times of their output
+ * tokens packed in request order (out_len[i] values each, int64 ns on one
+ * clock).  TTFT = first token - arrival; nTTFT = TTFT / input length; ITLs
+ * are the gaps between consecutive tokens, pooled over all requests; e2e =
+ * last token - arrival; throughput = output tokens / (last token - first
+ * arrival).  Medians take the mean of the two middle values for an even
+ * count; p90/p99 use the nearest-rank rule; NaN when there are no values.
+ * Pure host code; LP_EINVAL on null pointers, n < 1 or lengths < 1. */
+typedef struct {
+  int64_t n_requests, output_tokens, itl_count;
+  double ttft_p50_ns, nttft_p50_ns, itl_p50_ns, e2e_p50_ns;
+  double ttft_p90_ns, itl_p90_ns, itl_p99_ns;
+  double throughput_tok_s;
+} lp_latency_summary;
+
+int lp_summarize_latencies(int32_t n, const int64_t *arrival_ns, const int32_t *in_len, const int32_t *out_len,
+                           const int64_t *token_ns, lp_latency_summary *out);
+
+/* The same metrics over every request of the engine's last lp_run. */
+int lp_get_latency_summary(lp_engine *e, lp_latency_summary *out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -198,14 +198,16 @@ def median(values):
 
 
 def summarize(arrivals: dict, token_ns: dict, in_lens: dict):
-    """Median TTFT, nTTFT, pooled ITL, and throughput over one experiment."""
-    ttfts, nttfts, itls = [], [], []
+    """Median TTFT, nTTFT, pooled ITL and end-to-end latency, tail
+    percentiles, and throughput over one experiment (Sec. III-C-3)."""
+    ttfts, nttfts, itls, e2es = [], [], [], []
     n_tokens = 0
     for rid, times in token_ns.items():
-        ttft, itl, _ = request_latencies(arrivals[rid], times)
+        ttft, itl, e2e = request_latencies(arrivals[rid], times)
         ttfts.append(ttft)
         nttfts.append(ttft / in_lens[rid])
         itls.extend(itl)
+        e2es.append(e2e)
         n_tokens += len(times)
     start = min(arrivals.values())
     end = max(max(t) for t in token_ns.values())
@@ -213,8 +215,14 @@ def summarize(arrivals: dict, token_ns: dict, in_lens: dict):
         "ttft_p50_ns": median(ttfts),
         "nttft_p50_ns": median(nttfts),
         "itl_p50_ns": median(itls),
+        "e2e_p50_ns": median(e2es),
+        "ttft_p90_ns": percentile_nearest_rank(ttfts, 90),
+        "itl_p90_ns": percentile_nearest_rank(itls, 90),
+        "itl_p99_ns": percentile_nearest_rank(itls, 99),
         "throughput_tok_s": n_tokens / ((end - start) * 1e-9) if end > start else float("inf"),
         "output_tokens": n_tokens,
+        "n_requests": len(token_ns),
+        "itl_count": len(itls),
     }
 
 

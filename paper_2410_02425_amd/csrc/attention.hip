@@ -55,14 +55,18 @@ struct Vec8<float> {
 
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const T *__restrict__ q, RowMeta rows,
-                                                          KVCache kv, int layer, int n_heads,
+                                                          KVCache kv, int layer, int M, int n_heads,
                                                           int max_splits, float *__restrict__ ws) {
   constexpr int DPL = HD / 64;  // dims per lane in P.V
   __shared__ float qs[G][HD];
   __shared__ float ps[4][G][64];
   __shared__ float wm[4][G], wl[4][G];
   __shared__ float wo[4][G][HD];
-  const int s = blockIdx.x, g = blockIdx.y, m = blockIdx.z;
+  // one linear grid, KV head fastest and chunk slowest: the live chunks of
+  // short contexts are the low block ids, which the dispatcher spreads evenly
+  // over the XCDs, and the idle ones (past a row's context) come last
+  const int g = blockIdx.x % kv.n_kv_heads, m = (blockIdx.x / kv.n_kv_heads) % M;
+  const int s = blockIdx.x / (kv.n_kv_heads * M);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int slot = rows.row_slot[m];
   const int ctx = rows.row_pos[m] + 1;
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
 // of the block are requested before any is used.
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restrict__ q, RowMeta rows, KVCache kv,
-                                                               int layer, int n_heads, int max_splits,
+                                                               int layer, int M, int n_heads, int max_splits,
                                                                float *__restrict__ ws) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int KS = HD / 32;  // contraction steps over head_dim
@@ -199,7 +203,11 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
   __shared__ T pls[4][16][64 + 8];
   __shared__ float wm[4][16], wl[4][16];
   __shared__ float wo[4][G][HD];
-  const int s = blockIdx.x, g = blockIdx.y, m = blockIdx.z;
+  // one linear grid, KV head fastest and chunk slowest: the live chunks of
+  // short contexts are the low block ids, which the dispatcher spreads evenly
+  // over the XCDs, and the idle ones (past a row's context) come last
+  const int g = blockIdx.x % kv.n_kv_heads, m = (blockIdx.x / kv.n_kv_heads) % M;
+  const int s = blockIdx.x / (kv.n_kv_heads * M);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, quad = lane >> 4, kq = quad * 8;
   const int slot = rows.row_slot[m];
@@ -325,12 +333,12 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 }
 
 template <typename T, int HD, int G>
-static void launch_decode_group(dim3 grid, const T *q, const RowMeta &rows, const KVCache &kv, int layer,
+static void launch_decode_group(dim3 grid, const T *q, const RowMeta &rows, const KVCache &kv, int layer, int M,
                                 int n_heads, int splits, float *ws, hipStream_t s) {
   if constexpr (sizeof(T) == 2)
-    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws);
+    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, splits, ws);
   else
-    decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, n_heads, splits, ws);
+    decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, splits, ws);
 }
 
 template <typename T, int HD>
@@ -338,12 +346,12 @@ static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCa
                              int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
   const int G = n_heads / kv.n_kv_heads;
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
-  dim3 grid(splits, kv.n_kv_heads, M);
+  dim3 grid((unsigned)(splits * kv.n_kv_heads * M));
   switch (G) {
-    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
-    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
-    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
-    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, n_heads, splits, ws, s); break;
+    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
+    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
+    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
+    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
     default: return;
   }
   decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, splits, ws, out);

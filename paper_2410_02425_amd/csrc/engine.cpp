@@ -662,8 +662,7 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
     if (prefill)
       launch_prefill_attention<T>(qb, ab, dm.seq_start, dm.seq_slot, n_seq, max_len, kv, l, D.Hq, st);
     else
-      launch_decode_attention<T>(qb, ab, rows, kv, l, M, D.Hq, e->opt.max_seq_len, e->ptr<float>(e->Ly.attn_ws),
-                                 st);
+      launch_decode_attention<T>(qb, ab, rows, kv, l, M, D.Hq, max_len, e->ptr<float>(e->Ly.attn_ws), st);
     Epi eo{};
     eo.kind = EPI_RESID;
     eo.out = x;
@@ -759,6 +758,7 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
       const SReq &q = e->reqs[ri];
       h[o_slot + j] = ps.slots[j];
       h[o_pos + j] = ps.pos[j];
+      max_len = std::max(max_len, ps.pos[j] + 1);  // decode: the longest context
       // the token fed at position pos is output token number pos - in_len
       const int k = ps.pos[j] - q.in_len;
       const bool forced = e->forced_off[ri] >= 0 && k < e->forced_n[ri];
@@ -991,6 +991,21 @@ extern "C" int lp_get_token_times(lp_engine *e, int64_t id, int64_t *token_ns) {
   const auto &tt = e->out_times[it->second];
   memcpy(token_ns, tt.data(), tt.size() * 8);
   return LP_OK;
+}
+
+extern "C" int lp_get_latency_summary(lp_engine *e, lp_latency_summary *out) {
+  if (!e || !out) return LP_EINVAL;
+  if (!e->have_results) return e->err = "no results", LP_ESTATE;
+  const int32_t n = (int32_t)e->reqs.size();
+  std::vector<int64_t> arr(n), toks;
+  std::vector<int32_t> in(n), outl(n);
+  for (int32_t i = 0; i < n; ++i) {
+    arr[i] = e->out_arrival[i];
+    in[i] = e->reqs[i].in_len;
+    outl[i] = e->reqs[i].out_len;
+    toks.insert(toks.end(), e->out_times[i].begin(), e->out_times[i].end());
+  }
+  return lp_summarize_latencies(n, arr.data(), in.data(), outl.data(), toks.data(), out);
 }
 
 extern "C" int lp_get_run_stats(lp_engine *e, lp_run_stats *out) {

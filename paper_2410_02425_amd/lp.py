@@ -22,7 +22,7 @@ EXPORTED = [
     "lp_arena_bytes_required", "lp_engine_create", "lp_load_weights", "lp_init_weights_random",
     "lp_query_max_batch_weight", "lp_submit", "lp_set_forced_tokens", "lp_run", "lp_get_result",
     "lp_get_token_times", "lp_get_run_stats", "lp_get_step_log", "lp_get_logits", "lp_last_error",
-    "lp_engine_destroy", "lp_sched_simulate",
+    "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
     "lp_op_gemm", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
     "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight",
 ]
@@ -61,6 +61,16 @@ class RunStats(C.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+class LatencySummary(C.Structure):
+    _fields_ = [("n_requests", C.c_int64), ("output_tokens", C.c_int64), ("itl_count", C.c_int64),
+                ("ttft_p50_ns", C.c_double), ("nttft_p50_ns", C.c_double), ("itl_p50_ns", C.c_double),
+                ("e2e_p50_ns", C.c_double), ("ttft_p90_ns", C.c_double), ("itl_p90_ns", C.c_double),
+                ("itl_p99_ns", C.c_double), ("throughput_tok_s", C.c_double)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
 _lib = None
 
 
@@ -90,6 +100,8 @@ def lib():
             "lp_engine_destroy": [vp],
             "lp_sched_simulate": [P(Request), i32, i32, i64, i64, i32, i32, i64, i64, i64, i64, P(StepRecord),
                                   i64, P(i64), P(i64), P(i32), i64, P(i64), i64, P(i64)],
+            "lp_summarize_latencies": [i32, P(i64), P(i32), P(i32), P(i64), P(LatencySummary)],
+            "lp_get_latency_summary": [vp, P(LatencySummary)],
             "lp_op_gemm": [i32, vp, i64, vp, vp, i32, i32, i32, i32, vp, sz, vp],
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
             "lp_op_decode_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp, sz,
@@ -172,6 +184,7 @@ class Engine:
         if getattr(self, "h", None):
             lib().lp_engine_destroy(self.h)
             self.h = None
+        self.arena = None
 
     def __del__(self):
         try:
@@ -214,6 +227,12 @@ class Engine:
                                    itl.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(e2e), C.byref(arr)), self.h)
         return {"tokens": toks, "ttft_ns": ttft.value, "itl_ns": itl[: r.out_len - 1], "e2e_ns": e2e.value,
                 "arrival_ns": arr.value}
+
+    def latency_summary(self) -> dict:
+        """Load-test metrics of the last run over all submitted requests."""
+        out = LatencySummary()
+        _check(lib().lp_get_latency_summary(self.h, C.byref(out)), self.h)
+        return out.as_dict()
 
     def token_times(self, rid: int):
         r = self._reqs[rid]
@@ -286,6 +305,23 @@ def sched_simulate(reqs, max_batch, max_batch_weight, max_prefill_tokens, closed
         token_ns[int(q.id)] = toks[t:t + q.out_len].tolist()
         t += q.out_len
     return out, token_ns, {int(q.id): int(a) for q, a in zip(reqs, arrivals)}
+
+
+def summarize_latencies(arrival_ns, in_len, out_len, token_ns) -> dict:
+    """Load-test metrics of one experiment: per-request arrival times, input
+    and output lengths, and output-token times packed in request order."""
+    arr = np.ascontiguousarray(arrival_ns, dtype=np.int64)
+    inl = np.ascontiguousarray(in_len, dtype=np.int32)
+    outl = np.ascontiguousarray(out_len, dtype=np.int32)
+    toks = np.ascontiguousarray(token_ns, dtype=np.int64)
+    if toks.size != int(outl.sum()) or not (arr.size == inl.size == outl.size):
+        raise ValueError("token_ns must hold sum(out_len) values; one arrival and length per request")
+    out = LatencySummary()
+    _check(lib().lp_summarize_latencies(arr.size, arr.ctypes.data_as(C.POINTER(C.c_int64)),
+                                        inl.ctypes.data_as(C.POINTER(C.c_int32)),
+                                        outl.ctypes.data_as(C.POINTER(C.c_int32)),
+                                        toks.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(out)))
+    return out.as_dict()
 
 
 # ------------------------------------------------------------------ single-kernel ops (torch tensors)

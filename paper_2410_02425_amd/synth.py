@@ -293,12 +293,15 @@ def make_requests(wl: Workload, vocab: int, n_requests: int | None = None):
     """Seeded request list; lengths are drawn independently (the configs do not
     correlate input and output lengths)."""
     n = wl.n_requests if n_requests is None else n_requests
+    # the stream holds the workload's own count; asking for more extends it
+    # (the first wl.n_requests requests then differ from the stock ones)
+    m = max(n, wl.n_requests)
     _, rl, rp, ra = workload_seeds(wl.base_seed)
-    ins = _lengths(rl, wl.n_requests, wl.in_lognormal, wl.in_range, wl.fixed_in)[:n]
-    outs = _lengths(rl, wl.n_requests, wl.out_lognormal, wl.out_range, wl.fixed_out)[:n]
+    ins = _lengths(rl, m, wl.in_lognormal, wl.in_range, wl.fixed_in)[:n]
+    outs = _lengths(rl, m, wl.out_lognormal, wl.out_range, wl.fixed_out)[:n]
     arrivals = np.zeros(n, dtype=np.int64)
     if wl.mode == "open":
-        gaps = ra.exponential(1.0 / wl.rate_per_s, size=wl.n_requests)[:n]
+        gaps = ra.exponential(1.0 / wl.rate_per_s, size=m)[:n]
         arrivals = np.rint(np.cumsum(gaps) * 1e9).astype(np.int64)
     reqs = []
     for i in range(n):

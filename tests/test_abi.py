@@ -98,3 +98,53 @@ def test_scheduler_golden_schedule():
         assert [[s["kind"], s["ids"], s["slots"], s["end_ns"]] for s in steps] == c["steps"]
         assert {str(k): v for k, v in toks.items()} == c["token_ns"]
         assert {str(k): v for k, v in arr.items()} == c["arrival_ns"]
+
+
+SUMMARY_KEYS = ("n_requests", "output_tokens", "itl_count", "ttft_p50_ns", "nttft_p50_ns", "itl_p50_ns",
+                "e2e_p50_ns", "ttft_p90_ns", "itl_p90_ns", "itl_p99_ns", "throughput_tok_s")
+
+
+def _native_summary(reqs, arr, toks):
+    return lp.summarize_latencies([arr[r.id] for r in reqs], [r.in_len for r in reqs],
+                                  [r.out_len for r in reqs], np.concatenate([toks[r.id] for r in reqs]))
+
+
+def test_latency_summary_golden():
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "latency_example.json")) as f:
+        g = json.load(f)
+    rq = g["requests"]
+    got = lp.summarize_latencies([r["arrival_ns"] for r in rq], [r["in_len"] for r in rq],
+                                 [len(r["token_ns"]) for r in rq], np.concatenate([r["token_ns"] for r in rq]))
+    for k in SUMMARY_KEYS:
+        if k != "throughput_tok_s":
+            assert got[k] == g["expected"][k], k
+    assert got["throughput_tok_s"] == pytest.approx(g["expected"]["throughput_tok_s"], rel=1e-12)
+
+
+@pytest.mark.parametrize("closed", [True, False])
+def test_latency_summary_matches_oracle(closed):
+    """The native load-test metrics equal the oracle's, bit for bit, over
+    simulated schedules (odd and even counts, single-token requests)."""
+    rng = np.random.default_rng(21 if closed else 22)
+    for trial in range(30):
+        n = int(rng.integers(1, 30))
+        reqs, t = [], 0
+        for i in range(n):
+            t += int(rng.integers(0, 5000))
+            reqs.append(synth.Request(i, np.zeros(int(rng.integers(1, 60)), np.int32), int(rng.integers(1, 12)),
+                                      t if not closed else 0))
+        steps, toks, arr = lp.sched_simulate(reqs, int(rng.integers(1, 8)), 400, 300, closed,
+                                             int(rng.integers(1, 10)), 700, int(rng.integers(1, 9)), 300,
+                                             int(rng.integers(1, 40)))
+        got = _native_summary(reqs, arr, toks)
+        exp = S.summarize(arr, toks, {r.id: r.in_len for r in reqs})
+        for k in SUMMARY_KEYS:
+            assert (got[k] == exp[k]) or (np.isnan(got[k]) and np.isnan(exp[k])), (trial, k, got[k], exp[k])
+
+
+def test_latency_summary_rejects_bad_input():
+    with pytest.raises(lp.LPError):
+        lp.summarize_latencies([0], [0], [1], [5])
+    with pytest.raises(ValueError):
+        lp.summarize_latencies([0, 1], [1, 1], [2, 1], [5, 6])

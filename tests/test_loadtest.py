@@ -1,0 +1,87 @@
+"""Load-test procedures (Sec. III-C): the batch-weight search and corner-case
+batches on the host, and on the GPU the closed-loop characterization and the
+search's budget checked against engine creation."""
+import numpy as np
+import pytest
+
+from oracle import serving as S
+from paper_2410_02425_amd import loadtest, lp, synth
+
+
+@pytest.mark.parametrize("name,gb", [("8b", 40), ("8b", 100), ("8b", 250), ("7b", 60), ("tiny", 1)])
+def test_search_max_batch_weight_is_the_largest_fitting_budget(name, gb):
+    shape, wl = synth.SHAPES[name], synth.WORKLOADS[name]
+    cfg = lp.make_config(shape)
+    opt = loadtest._options(wl, wl.max_batch)
+    arena = int(gb * 2**30)
+    w = loadtest.search_max_batch_weight(cfg, opt, arena)
+    assert w > 0 and w % loadtest.KV_BLOCK == 0
+
+    def need(x):
+        return lp.arena_bytes(cfg, lp.EngineOptions(opt.max_batch, opt.max_seq_len, x, opt.max_prefill_tokens, 0, 0))
+
+    assert need(w) <= arena < need(w + loadtest.KV_BLOCK)
+    # the KV pool grows by exactly the cache bytes of the added tokens
+    assert need(w + loadtest.KV_BLOCK) - need(w) == loadtest.KV_BLOCK * loadtest.kv_bytes_per_token(cfg)
+
+
+def test_search_reports_zero_when_weights_do_not_fit():
+    cfg = lp.make_config(synth.SHAPES["8b"])
+    assert loadtest.search_max_batch_weight(cfg, loadtest._options(synth.WORKLOADS["8b"], 64), 8 * 2**30) == 0
+
+
+@pytest.mark.parametrize("weight,max_batch", [(100000, 64), (20000, 4), (5120, 8), (3000, 8), (10**7, 64)])
+def test_corner_case_batch(weight, max_batch):
+    reqs = loadtest.corner_case_requests(weight, max_batch, 5120, 1000)
+    total = sum(r.in_len + r.out_len for r in reqs)
+    assert 1 <= len(reqs) <= max_batch and total <= max(weight, 5120)
+    if weight >= 5120:
+        assert all(r.in_len + r.out_len == 5120 for r in reqs)
+        assert len(reqs) == min(max_batch, weight // 5120)
+    else:
+        assert len(reqs) == 1 and total == weight
+
+
+# ------------------------------------------------------------------ GPU
+
+@pytest.mark.gpu
+def test_characterize_tiny_matches_oracle_accounting():
+    import torch
+    torch.cuda.set_device(0)
+    shape, wl = synth.SHAPES["tiny"], synth.WORKLOADS["tiny"]
+    cfg = lp.make_config(shape)
+    eng = lp.Engine(cfg, lp.EngineOptions(4, 64, 0, 4096, 0, 0))
+    eng.init_weights_random(3, 0.02)
+    rows = loadtest.characterize(eng, wl, shape.vocab, [1, 2, 4], requests_per_user=2)
+    assert [r["users"] for r in rows] == [1, 2, 4]
+    for r in rows:
+        U = r["users"]
+        # replay the last run (U users) through the oracle's accounting
+        reqs = synth.make_requests(wl, shape.vocab, max(2 * U, 4))
+        eng.submit(reqs)
+        eng.run(lp.LP_CLOSED_LOOP, U)
+        got = eng.latency_summary()
+        res = {q.id: eng.result(q.id) for q in reqs}
+        toks = {q.id: eng.token_times(q.id).tolist() for q in reqs}
+        exp = S.summarize({q.id: res[q.id]["arrival_ns"] for q in reqs}, toks, {q.id: q.in_len for q in reqs})
+        for k in ("ttft_p50_ns", "nttft_p50_ns", "itl_p50_ns", "e2e_p50_ns", "itl_p90_ns", "output_tokens",
+                  "throughput_tok_s"):
+            assert got[k] == exp[k], (U, k)
+        assert max(st["n_rows"] for st in eng.step_log()) <= U
+        assert r["output_tokens"] == sum(q.out_len for q in reqs)
+    eng.close()
+
+
+@pytest.mark.gpu
+def test_searched_budget_runs_and_one_block_more_does_not_fit():
+    import torch
+    torch.cuda.set_device(0)
+    cfg = lp.make_config(synth.SHAPES["tiny"])
+    opt = lp.EngineOptions(4, 96, 0, 4096, 0, 0)
+    arena = lp.arena_bytes(cfg, lp.EngineOptions(4, 96, 640, 4096, 0, 0)) + 1000
+    w = loadtest.search_max_batch_weight(cfg, opt, arena)
+    assert w == 640
+    ok, msg = loadtest.verify_batch_weight(cfg, opt, w, arena)
+    assert ok, msg
+    ok, msg = loadtest.verify_batch_weight(cfg, opt, w + loadtest.KV_BLOCK, arena)
+    assert not ok and "-2" in msg  # LP_ENOMEM

@@ -27,7 +27,8 @@ def test_latency_golden_example():
         assert (ttft, itl, e2e) == (exp["ttft"], exp["itl"], exp["e2e"])
         assert ttft / r["in_len"] == exp["nttft"]
     s = S.summarize(arr, toks, ins)
-    for k in ("ttft_p50_ns", "nttft_p50_ns", "itl_p50_ns", "output_tokens"):
+    for k in ("ttft_p50_ns", "nttft_p50_ns", "itl_p50_ns", "output_tokens", "e2e_p50_ns", "ttft_p90_ns",
+              "itl_p90_ns", "itl_p99_ns", "n_requests", "itl_count"):
         assert s[k] == g["expected"][k]
     assert s["throughput_tok_s"] == pytest.approx(g["expected"]["throughput_tok_s"], rel=1e-12)
 
