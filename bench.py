@@ -39,8 +39,9 @@ MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16
 # 16928 gate/up dispatches of all row counts) and scaled by what the same
 # counters read for a plain 1 GiB device copy: FETCH_SIZE x2.0 (it reads
 # 524302 KiB for 1048576 KiB fetched), WRITE_SIZE x1.0.  The figure holds for
-# the kernel source it was measured on and is dropped when that changes.
-GATE_UP_TRAFFIC = {"bytes_per_launch": 238673243, "kernel_source": "80cb41b9d22c0ae5",
+# the kernel source and launch plan it was measured on and is dropped when
+# they change.
+GATE_UP_TRAFFIC = {"bytes_per_launch": 238531905, "kernel_source": "98317d0dfb6faad6",
                    "profile": "profiles/decode_gate_up_gemm_8b.md"}
 
 
