@@ -154,18 +154,30 @@ def test_tiny_bf16_teacher_forced_logits(act):
         assert np.max(np.abs(got - ref[r.id])) <= TOL[act]
 
 
-@pytest.mark.parametrize("act", [0, lp.LP_FLAG_BF16_ACTIVATIONS])
-def test_8b_shape_two_layers_full_width_teacher_forced(act):
-    """8B-shape GQA at full width (d=4096, 32/8 heads, F=14336, V=128256),
-    2 layers, device-generated weights; logits compared on 2048 sampled vocab
-    rows plus the GPU's argmax (teacher forcing keeps both on one sequence)."""
-    shape = synth.SHAPES["8b"].with_layers(2)
+# Full-width shapes of every bf16 configuration at reduced depth: 8B (GQA,
+# 4 query heads per KV head), 7B and 13B (MHA: one), 70B (8 per KV head,
+# d = 8192).  (name, layers, prompt lengths, activation flags).
+FULL_WIDTH_CASES = [
+    ("8b", 2, [67, 1, 300], 0),
+    ("8b", 2, [67, 1, 300], lp.LP_FLAG_BF16_ACTIVATIONS),
+    ("7b", 1, [67, 1, 130], 0),
+    ("13b", 1, [40, 1, 90], 0),
+    ("70b", 1, [40, 1, 90], 0),
+]
+
+
+@pytest.mark.parametrize("name,layers,lens,act", FULL_WIDTH_CASES)
+def test_full_width_teacher_forced(name, layers, lens, act):
+    """A configuration's shape at full width and reduced depth, device-generated
+    weights; logits compared on 2048 sampled vocab rows plus the GPU's argmax
+    (teacher forcing keeps both on one sequence)."""
+    shape = synth.SHAPES[name].with_layers(layers)
     seed = 0x8B8B
     rng = np.random.default_rng(4)
-    reqs = [synth.Request(0, rng.integers(0, shape.vocab, size=67).astype(np.int32), 3),
-            synth.Request(1, rng.integers(0, shape.vocab, size=1).astype(np.int32), 3),
-            synth.Request(2, rng.integers(0, shape.vocab, size=300).astype(np.int32), 2)]
-    forced = {0: [5, 127000], 1: [99, 1], 2: [42]}
+    outs = [3, 3, 2]
+    reqs = [synth.Request(i, rng.integers(0, shape.vocab, size=n).astype(np.int32), o)
+            for i, (n, o) in enumerate(zip(lens, outs))]
+    forced = {0: [5, shape.vocab - 1], 1: [99, 1], 2: [42]}
     eng = engine_for(shape, 4, 512, flags=lp.LP_FLAG_KEEP_LOGITS | act, max_prefill=1024)
     eng.init_weights_random(seed, 0.02)
     eng.submit(reqs)
@@ -177,15 +189,16 @@ def test_8b_shape_two_layers_full_width_teacher_forced(act):
     w = {}
     vocab_rows = np.unique(np.concatenate([rng.integers(0, shape.vocab, 2048), [0, shape.vocab - 1]]))
     used = np.unique(np.concatenate([r.prompt for r in reqs] + [np.array(v) for v in forced.values()]))
-    for name, tid, (rows, cols) in names:
-        if name == "embed":  # only the rows of the tokens fed; ids remapped below
-            w[name] = synth.tensor_values(seed, tid, used, cols, 0.02, shape.dtype)
-        elif name == "lm_head":
+    for nm, tid, (rows, cols) in names:
+        if nm == "embed":  # only the rows of the tokens fed; ids remapped below
+            w[nm] = synth.tensor_values(seed, tid, used, cols, 0.02, shape.dtype)
+        elif nm == "lm_head":
             continue
         else:
-            v = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02, shape.dtype, gain=synth.is_gain(name))
-            w[name] = v.reshape(cols) if rows == 1 else v
+            v = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02, shape.dtype, gain=synth.is_gain(nm))
+            w[nm] = v.reshape(cols) if rows == 1 else v
     got_all = {r.id: np.stack([eng.logits(r.id, k) for k in range(r.out_len)]) for r in reqs}
+    eng.close()
     gpu_top = {rid: np.argmax(g, axis=1) for rid, g in got_all.items()}
     extra = np.unique(np.concatenate(list(gpu_top.values())))
     rows_needed = np.unique(np.concatenate([vocab_rows, extra]))
@@ -198,7 +211,7 @@ def test_8b_shape_two_layers_full_width_teacher_forced(act):
         ref = T.forward(m, toks_in, T.KVCache(m), "all")[r.in_len - 1:]
         got = got_all[r.id][:, rows_needed]
         err = np.max(np.abs(got - ref))
-        print(f"request {r.id}: max |logit error| on {rows_needed.size} rows = {err:.3e}")
+        print(f"{name} x{layers} request {r.id}: max |logit error| on {rows_needed.size} rows = {err:.3e}")
         assert err <= TOL[act]
         # the GPU's greedy choice is (within tolerance) the oracle's best among the sampled rows
         pos = np.searchsorted(rows_needed, gpu_top[r.id])
