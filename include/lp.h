@@ -219,6 +219,42 @@ int lp_summarize_latencies(int32_t n, const int64_t *arrival_ns, const int32_t *
 /* The same metrics over every request of the engine's last lp_run. */
 int lp_get_latency_summary(lp_engine *e, lp_latency_summary *out);
 
+/* ------------------------------------------------------------------------
+ * Workload generator (Sec. III-B): a non-parametric joint model of request
+ * parameters.  Pure host code.
+ *
+ * lp_wg_fit: records [n][n_params] row-major doubles (one row per trace
+ * request, finite).  Each parameter is binned into at most max_bins (the
+ * paper uses 64) intervals of about equal record counts, or one bin per
+ * distinct value when it has at most max_bins of them.  With sorted values
+ * v[0..n-1] and more distinct values than bins, the lower edges are v[0]
+ * then v[ceil(j n / max_bins)] for j = 1..max_bins-1 (0-based), equal edges
+ * merging; bin i is [edge_i, edge_{i+1}) (the last closed at v[n-1]) and its
+ * centre is the midpoint.  The model keeps the sparse histogram of the
+ * multi-dimensional bins the records fall in.  *out is owned by the caller
+ * (lp_wg_free).  LP_EINVAL on bad sizes or non-finite values.
+ *
+ * lp_wg_info: n_bins of parameter `param` (param = -1: none) and the number
+ * of non-empty multi-dimensional bins.
+ * lp_wg_bins: the parameter's edges [n_bins + 1], centres [n_bins] and record
+ * counts [n_bins] (any may be NULL).
+ *
+ * lp_wg_sample: n requests from n uniforms u[s] in [0, 1): with N records,
+ * r = floor(u N) picks the first multi-dimensional bin, in lexicographic
+ * order of bin indices, whose cumulative count exceeds r; out [n][n_params]
+ * receives the centres of that bin's intervals, joint_bin [n] (optional) its
+ * index in that order.
+ * lp_wg_sample_independent: the same from each parameter's own marginal
+ * histogram, u [n][n_params] (one uniform per parameter): the independent-
+ * parameter baseline the paper compares against (Sec. IV-A). */
+typedef struct lp_wg_model lp_wg_model;
+int lp_wg_fit(const double *records, int64_t n, int32_t n_params, int32_t max_bins, lp_wg_model **out);
+int lp_wg_info(const lp_wg_model *m, int32_t param, int32_t *n_bins, int64_t *n_joint_bins);
+int lp_wg_bins(const lp_wg_model *m, int32_t param, double *edges, double *centres, int64_t *counts);
+int lp_wg_sample(const lp_wg_model *m, const double *u, int64_t n, double *out, int64_t *joint_bin);
+int lp_wg_sample_independent(const lp_wg_model *m, const double *u, int64_t n, double *out);
+void lp_wg_free(lp_wg_model *m);
+
 #ifdef __cplusplus
 }
 #endif

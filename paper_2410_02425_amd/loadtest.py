@@ -11,6 +11,10 @@ inference service (Sec. III-C).
   corner-case batch of maximal-length requests that fills the budget.
 * ``batch_weight_sweep``: end-to-end latency and throughput of one load test
   run under a range of batch-weight budgets.
+* ``generated_requests`` / ``generator_comparison``: requests from the
+  workload generator's joint request model (Sec. III-B), or with every
+  parameter drawn from its own marginal, and the load tests of the two
+  (the comparison of Sec. IV-A).
 
 Every step of a test runs in the engine behind the C ABI (scheduling, the
 GPU serving step, timestamps and the latency summary); this module only
@@ -140,6 +144,46 @@ def batch_weight_sweep(cfg: lp.ModelConfig, wl: synth.Workload, weights, users: 
     return rows
 
 
+def generated_requests(model: lp.RequestModel, uniforms, vocab: int, max_in: int, max_out: int, corpus,
+                       independent: bool = False):
+    """Engine requests from workload-generator samples (columns as
+    synth.TRACE_COLUMNS).  Token counts are the sampled interval centres
+    rounded to the nearest integer (ties to even) and clipped to the engine's
+    limits; the prompt is the corpus truncated to that length (Sec. III-B); a
+    request with batch size b becomes b sequences submitted together.  The
+    sampling parameters are carried by the model but the engine decodes
+    greedily."""
+    vals = model.sample_independent(uniforms) if independent else model.sample(uniforms)[0]
+    reqs = []
+    for row in vals:
+        n_in = int(np.clip(np.rint(row[0]), 1, max_in))
+        n_out = int(np.clip(np.rint(row[1]), 1, max_out))
+        for _ in range(int(np.clip(np.rint(row[2]), 1, 64))):
+            reqs.append(synth.Request(len(reqs), np.ascontiguousarray(corpus[:n_in]), n_out))
+    return reqs
+
+
+def generator_comparison(eng: lp.Engine, model: lp.RequestModel, users, n_per_user: int, seed: int):
+    """Closed-loop load tests with requests from the joint model and from
+    independent marginals, the same number of generated requests for both."""
+    rng = np.random.default_rng(seed)
+    corpus = rng.integers(0, eng.cfg.vocab, size=eng.opt.max_seq_len).astype(np.int32)
+    max_out = min(1500, eng.opt.max_seq_len // 2)  # the traces' output range (Table II)
+    max_in = eng.opt.max_seq_len - max_out
+    rows = []
+    for U in users:
+        n = max(n_per_user * U, 4)
+        u_joint = rng.random(n)
+        u_ind = rng.random((n, model.n_params))
+        for mode, reqs in (("joint", generated_requests(model, u_joint, eng.cfg.vocab, max_in, max_out, corpus)),
+                           ("independent", generated_requests(model, u_ind, eng.cfg.vocab, max_in, max_out, corpus,
+                                                              independent=True))):
+            eng.submit(reqs)
+            eng.run(lp.LP_CLOSED_LOOP, U)
+            rows.append({"mode": mode, "users": U, "generated": n, **eng.latency_summary()})
+    return rows
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -154,6 +198,11 @@ def main(argv=None):
     b.add_argument("--weights", default="8192,16384,32768,65536,131072,max",
                    help="budgets in tokens; 'max' is the searched maximum")
     b.add_argument("--arena-gb", type=float, default=0.0, help="memory budget (default: 85%% of free HBM)")
+    g = sub.add_parser("generator", help="joint vs independent request parameters (workload generator)")
+    g.add_argument("--config", default="8b")
+    g.add_argument("--users", default="4,16,64")
+    g.add_argument("--requests-per-user", type=int, default=2)
+    g.add_argument("--trace-records", type=int, default=200000)
     args = ap.parse_args(argv)
 
     import torch
@@ -161,6 +210,27 @@ def main(argv=None):
     shape, wl = synth.SHAPES[args.config], synth.WORKLOADS[args.config]
     cfg = lp.make_config(shape)
     key = synth.workload_seeds(wl.base_seed)[0]
+    if args.cmd == "generator":
+        import time
+        recs = synth.trace_records(wl.base_seed, args.trace_records)
+        t0 = time.perf_counter()
+        model = lp.RequestModel(recs, 64)
+        t_fit = time.perf_counter() - t0
+        u = np.random.default_rng(0).random(1000)
+        t0 = time.perf_counter()
+        model.sample(u)
+        t_draw = time.perf_counter() - t0
+        print(json.dumps({"config": args.config, "trace_records": args.trace_records,
+                          "joint_bins_nonempty": model.n_joint_bins(),
+                          "joint_bins_possible": int(np.prod([len(model.bins(p)[1]) for p in range(model.n_params)])),
+                          "fit_s": round(t_fit, 4), "draw_1000_ms": round(t_draw * 1e3, 4)}), flush=True)
+        users = [int(x) for x in args.users.split(",")]
+        eng = lp.Engine(cfg, lp.EngineOptions(max(users), 4096 + 1500, 0, 65536, 0, 0))
+        eng.init_weights_random(key, 0.02)
+        for row in generator_comparison(eng, model, users, args.requests_per_user, wl.base_seed):
+            print(json.dumps({"config": args.config, **row}), flush=True)
+        eng.close()
+        return 0
     if args.cmd == "characterize":
         users = [int(u) for u in args.users.split(",")]
         eng = lp.Engine(cfg, _options(wl, max(users)))

@@ -23,6 +23,7 @@ EXPORTED = [
     "lp_query_max_batch_weight", "lp_submit", "lp_set_forced_tokens", "lp_run", "lp_get_result",
     "lp_get_token_times", "lp_get_run_stats", "lp_get_step_log", "lp_get_logits", "lp_last_error",
     "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
+    "lp_wg_fit", "lp_wg_info", "lp_wg_bins", "lp_wg_sample", "lp_wg_sample_independent", "lp_wg_free",
     "lp_op_gemm", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
     "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight",
 ]
@@ -101,6 +102,11 @@ def lib():
             "lp_sched_simulate": [P(Request), i32, i32, i64, i64, i32, i32, i64, i64, i64, i64, P(StepRecord),
                                   i64, P(i64), P(i64), P(i32), i64, P(i64), i64, P(i64)],
             "lp_summarize_latencies": [i32, P(i64), P(i32), P(i32), P(i64), P(LatencySummary)],
+            "lp_wg_fit": [P(C.c_double), i64, i32, i32, P(vp)],
+            "lp_wg_info": [vp, i32, P(i32), P(i64)],
+            "lp_wg_bins": [vp, i32, P(C.c_double), P(C.c_double), P(i64)],
+            "lp_wg_sample": [vp, P(C.c_double), i64, P(C.c_double), P(i64)],
+            "lp_wg_sample_independent": [vp, P(C.c_double), i64, P(C.c_double)],
             "lp_get_latency_summary": [vp, P(LatencySummary)],
             "lp_op_gemm": [i32, vp, i64, vp, vp, i32, i32, i32, i32, vp, sz, vp],
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
@@ -119,6 +125,8 @@ def lib():
         L.lp_op_decode_attention_ws_bytes.argtypes = [i32, i32, i32, i32]
         L.lp_op_decode_attention_ws_bytes.restype = sz
         L.lp_engine_destroy.restype = None
+        L.lp_wg_free.argtypes = [vp]
+        L.lp_wg_free.restype = None
         _lib = L
     return _lib
 
@@ -322,6 +330,62 @@ def summarize_latencies(arrival_ns, in_len, out_len, token_ns) -> dict:
                                         outl.ctypes.data_as(C.POINTER(C.c_int32)),
                                         toks.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(out)))
     return out.as_dict()
+
+
+class RequestModel:
+    """The workload generator's joint request model (Sec. III-B), fitted to
+    trace records [n x n_params]; sampling takes the uniforms it consumes."""
+
+    def __init__(self, records, max_bins: int = 64):
+        rec = np.ascontiguousarray(records, dtype=np.float64)
+        if rec.ndim != 2:
+            raise ValueError("records must be [n, n_params]")
+        self.n_params = rec.shape[1]
+        h = C.c_void_p()
+        _check(lib().lp_wg_fit(rec.ctypes.data_as(C.POINTER(C.c_double)), rec.shape[0], self.n_params, max_bins,
+                               C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None):
+            lib().lp_wg_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        self.close()
+
+    def n_joint_bins(self) -> int:
+        nj = C.c_int64()
+        _check(lib().lp_wg_info(self.h, -1, None, C.byref(nj)))
+        return nj.value
+
+    def bins(self, param: int):
+        """(edges [n_bins + 1], centres [n_bins], record counts [n_bins])."""
+        nb = C.c_int32()
+        _check(lib().lp_wg_info(self.h, param, C.byref(nb), None))
+        e, c = np.zeros(nb.value + 1), np.zeros(nb.value)
+        k = np.zeros(nb.value, dtype=np.int64)
+        _check(lib().lp_wg_bins(self.h, param, e.ctypes.data_as(C.POINTER(C.c_double)),
+                                c.ctypes.data_as(C.POINTER(C.c_double)), k.ctypes.data_as(C.POINTER(C.c_int64))))
+        return e, c, k
+
+    def sample(self, u):
+        """Requests [n x n_params] and their joint-bin indices for uniforms u [n]."""
+        uu = np.ascontiguousarray(u, dtype=np.float64).reshape(-1)
+        out = np.zeros((uu.size, self.n_params))
+        jb = np.zeros(uu.size, dtype=np.int64)
+        _check(lib().lp_wg_sample(self.h, uu.ctypes.data_as(C.POINTER(C.c_double)), uu.size,
+                                  out.ctypes.data_as(C.POINTER(C.c_double)), jb.ctypes.data_as(C.POINTER(C.c_int64))))
+        return out, jb
+
+    def sample_independent(self, u):
+        """Requests [n x n_params] with every parameter drawn from its own
+        marginal, for uniforms u [n x n_params]."""
+        uu = np.ascontiguousarray(u, dtype=np.float64).reshape(-1, self.n_params)
+        out = np.zeros(uu.shape)
+        _check(lib().lp_wg_sample_independent(self.h, uu.ctypes.data_as(C.POINTER(C.c_double)), uu.shape[0],
+                                              out.ctypes.data_as(C.POINTER(C.c_double))))
+        return out
 
 
 # ------------------------------------------------------------------ single-kernel ops (torch tensors)

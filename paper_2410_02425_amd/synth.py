@@ -312,3 +312,44 @@ def make_requests(wl: Workload, vocab: int, n_requests: int | None = None):
 
 def uniform_f32(rng: np.random.Generator, shape, lo=-1.0, hi=1.0) -> np.ndarray:
     return rng.uniform(lo, hi, size=shape).astype(np.float32)
+
+
+# ---------------------------------------------------------------- trace stand-in
+
+# Columns of a synthetic trace record: the request parameters the paper finds
+# matter most for latency (Sec. III-A): token counts, the number of prompts in
+# the request, and the sampling parameters.
+TRACE_COLUMNS = ("in_tokens", "out_tokens", "batch_size", "sampling", "temperature", "top_k")
+
+# Rank correlation of the latent normals (Gaussian copula) behind the columns.
+# The production traces are unavailable; the paper reports that input tokens,
+# output tokens and batch size are strongly correlated with one another
+# (Sec. III-A).  These values are a stand-in with that structure.
+TRACE_CORRELATION = np.array([
+    # in    out   batch  samp  temp  topk
+    [1.00, 0.45, -0.50, 0.10, 0.00, 0.00],
+    [0.45, 1.00, -0.35, 0.30, 0.00, 0.00],
+    [-0.50, -0.35, 1.00, 0.00, 0.00, 0.00],
+    [0.10, 0.30, 0.00, 1.00, 0.00, 0.00],
+    [0.00, 0.00, 0.00, 0.00, 1.00, 0.50],
+    [0.00, 0.00, 0.00, 0.00, 0.50, 1.00],
+])
+
+
+def trace_records(seed: int, n: int) -> np.ndarray:
+    """n synthetic trace requests [n x 6] (TRACE_COLUMNS), seeded: input
+    tokens lognormal(6.0, 0.9) in [1, 4093], output tokens lognormal(4.8, 0.9)
+    in [1, 1500] (the ranges of the paper's Table II), batch size 1..5 (79%
+    single prompts), greedy or sampling decoding (38% sampling), and for
+    sampling requests a temperature in [0.05, 1.5] (two decimals) and top-k
+    in {5, 10, 20, 40, 50, 100} (0 and 0 for greedy)."""
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((n, 6)) @ np.linalg.cholesky(TRACE_CORRELATION).T
+    inp = np.clip(np.rint(np.exp(6.0 + 0.9 * z[:, 0])), 1, 4093)
+    out = np.clip(np.rint(np.exp(4.8 + 0.9 * z[:, 1])), 1, 1500)
+    batch = 1.0 + (z[:, 2] > 0.8) + (z[:, 2] > 1.4) + (z[:, 2] > 1.9) + (z[:, 2] > 2.3)
+    sampling = (z[:, 3] > 0.3).astype(np.float64)
+    temp = np.where(sampling > 0, np.round(np.clip(0.7 + 0.25 * z[:, 4], 0.05, 1.5), 2), 0.0)
+    topk = np.where(sampling > 0, np.array([5, 10, 20, 40, 50, 100.0])[np.digitize(z[:, 5], [-1, -0.3, 0.3, 1, 1.6])],
+                    0.0)
+    return np.stack([inp, out, batch, sampling, temp, topk], axis=1)

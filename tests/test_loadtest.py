@@ -85,3 +85,39 @@ def test_searched_budget_runs_and_one_block_more_does_not_fit():
     assert ok, msg
     ok, msg = loadtest.verify_batch_weight(cfg, opt, w + loadtest.KV_BLOCK, arena)
     assert not ok and "-2" in msg  # LP_ENOMEM
+
+
+def test_generated_requests_follow_the_samples():
+    model = lp.RequestModel(synth.trace_records(5, 20000))
+    rng = np.random.default_rng(0)
+    corpus = rng.integers(0, 1000, size=600).astype(np.int32)
+    u = rng.random(300)
+    vals, _ = model.sample(u)
+    reqs = loadtest.generated_requests(model, u, 1000, 500, 100, corpus)
+    assert len(reqs) == int(np.clip(np.rint(vals[:, 2]), 1, 64).sum())
+    k = 0
+    for row in vals:
+        for _ in range(int(np.rint(row[2]))):
+            r = reqs[k]
+            assert r.in_len == int(np.clip(np.rint(row[0]), 1, 500)) and r.out_len == int(np.clip(np.rint(row[1]), 1, 100))
+            assert np.array_equal(r.prompt, corpus[:r.in_len])
+            k += 1
+    ind = loadtest.generated_requests(model, rng.random((300, 6)), 1000, 500, 100, corpus, independent=True)
+    assert all(1 <= r.in_len <= 500 and 1 <= r.out_len <= 100 for r in ind)
+
+
+@pytest.mark.gpu
+def test_generator_comparison_tiny():
+    import torch
+    torch.cuda.set_device(0)
+    shape = synth.SHAPES["tiny"]
+    eng = lp.Engine(lp.make_config(shape), lp.EngineOptions(4, 128, 0, 4096, 0, 0))
+    eng.init_weights_random(5, 0.02)
+    model = lp.RequestModel(synth.trace_records(6, 5000), 64)
+    rows = loadtest.generator_comparison(eng, model, [1, 4], 2, 7)
+    assert [(r["mode"], r["users"]) for r in rows] == [("joint", 1), ("independent", 1), ("joint", 4),
+                                                        ("independent", 4)]
+    for r in rows:
+        assert r["output_tokens"] >= r["n_requests"] >= r["generated"]
+        assert r["throughput_tok_s"] > 0
+    eng.close()
