@@ -151,6 +151,16 @@ int lp_submit(lp_engine *e, const lp_request *reqs, int32_t n);
 /* Teacher forcing (parity checks only): the k-th decode step of request `id`
  * feeds toks[k] instead of the token it produced (n <= out_len - 1).  Call
  * after lp_submit. */
+/* Sampling parameters of a submitted request (Sec. III-A lists temperature,
+ * top-k and top-p among the request parameters that matter for latency);
+ * requests are greedy until this is called.  temperature 0 or top_p 0:
+ * greedy; top_k 0: no top-k limit; top_p >= 1: no nucleus limit.  The draw
+ * for output token k uses Philox4x32-10 with key (seed low, seed high) and
+ * counter (id low, id high, k, 0x53414D50); the choice rule is that of
+ * lp_op_sample (include/lp_ops.h).  LP_EINVAL for an unknown id or negative
+ * values. */
+int lp_set_sampling(lp_engine *e, int64_t id, float temperature, int32_t top_k, float top_p, uint64_t seed);
+
 int lp_set_forced_tokens(lp_engine *e, int64_t id, const int32_t *toks, int32_t n);
 
 /* Serves every submitted request to completion.  mode LP_CLOSED_LOOP: the

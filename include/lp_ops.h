@@ -72,6 +72,33 @@ int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t 
 int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_t tensor_id, int64_t rows, int64_t cols,
                       float std, void *hip_stream);
 
+/* Sampling parameters of one row (requests carry them, Sec. III-A):
+ * temperature <= 0 or top_p <= 0 mean greedy; top_k 0 means no top-k limit;
+ * top_p >= 1 means no nucleus limit; key / counter: the Philox4x32-10 key
+ * and the first three counter words of the row's random draw (the fourth is
+ * the constant 0x53414D50). */
+typedef struct {
+  float temperature;
+  int32_t top_k;
+  float top_p;
+  uint32_t key[2];
+  uint32_t counter[3];
+} lp_sample_params;
+
+/* Next token of each of M rows of fp32 logits (row stride ld >= V) under its
+ * sampling parameters; tokens [M] int32 (device).  Greedy rows take the
+ * lowest index among the maxima.  Otherwise, with m the row maximum:
+ * candidates are all tokens, or for 0 < top_k < V the tokens whose logit is
+ * at least the top_k-th largest (ties kept); a candidate's weight is
+ * q = floor(exp((logit - m) / temperature) * 2^40); for top_p < 1 the kept
+ * candidates are those with q >= t, t the largest value whose heavier-or-
+ * equal candidates weigh at least ceil(Z * floor(top_p * 2^24) / 2^24) (Z the
+ * candidates' total); the draw r = floor(Z_kept * u24 / 2^24), u24 the first
+ * Philox output word >> 8, picks the kept candidate, in vocabulary order,
+ * whose cumulative weight interval holds r. */
+int lp_op_sample(const float *logits, int64_t ld, int32_t M, int32_t V, const lp_sample_params *params,
+                 int32_t *tokens, void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

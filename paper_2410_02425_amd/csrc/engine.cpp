@@ -140,8 +140,10 @@ Layout plan_layout(const lp_model_config &c, const lp_engine_options &o, int64_t
   Ly.rope_cos = take((size_t)max_pos * (D.hd / 2) * 4);
   Ly.rope_sin = take((size_t)max_pos * (D.hd / 2) * 4);
   const int max_blocks = (o.max_seq_len + KV_BLOCK - 1) / KV_BLOCK;
-  // seven regions, each padded to 64 ints
-  Ly.meta_bytes = (size_t)(3 * R + 4 * (o.max_batch + 1) + (int64_t)o.max_batch * max_blocks + 7 * 64) * 4;
+  // eight regions, each padded to 64 ints: row slot / position / token,
+  // sequence starts / slots / LM rows, block table, sampling parameters
+  Ly.meta_bytes =
+      (size_t)(3 * R + 4 * (o.max_batch + 1) + (int64_t)o.max_batch * max_blocks + 8 * o.max_batch + 8 * 64) * 4;
   Ly.meta = take(Ly.meta_bytes);
   Ly.slot_tok = take((size_t)o.max_batch * 4);
   Ly.tok_log = take((size_t)TOKLOG_CAP * 4);
@@ -210,6 +212,7 @@ struct lp_engine {
   std::vector<int64_t> prompt_off;   // into the device pool
   std::vector<int64_t> forced_off;   // -1: none
   std::vector<int32_t> forced_n;
+  std::vector<SampleParams> sampling;  // per request (temperature 0: greedy)
   int64_t pool_used = 0;
   std::vector<int32_t> host_pool;
 
@@ -572,7 +575,23 @@ extern "C" int lp_submit(lp_engine *e, const lp_request *reqs, int32_t n) {
   e->pool_used = (int64_t)e->host_pool.size();
   e->forced_off.assign(n, -1);
   e->forced_n.assign(n, 0);
+  e->sampling.assign(n, SampleParams{});
   e->have_results = false;
+  return LP_OK;
+}
+
+extern "C" int lp_set_sampling(lp_engine *e, int64_t id, float temperature, int32_t top_k, float top_p,
+                               uint64_t seed) {
+  if (!e) return LP_EINVAL;
+  auto it = e->by_id.find(id);
+  if (it == e->by_id.end()) return e->err = "unknown request id", LP_EINVAL;
+  if (!(temperature >= 0.f) || top_k < 0 || !(top_p >= 0.f)) return e->err = "sampling parameters", LP_EINVAL;
+  SampleParams &sp = e->sampling[it->second];
+  sp.temperature = temperature;
+  sp.top_k = top_k;
+  sp.top_p = top_p;
+  sp.key[0] = (uint32_t)seed;
+  sp.key[1] = (uint32_t)(seed >> 32);
   return LP_OK;
 }
 
@@ -599,6 +618,7 @@ namespace {
 
 struct StepMeta {
   int32_t *row_slot, *row_pos, *row_tok, *seq_start, *seq_slot, *lm_rows, *block_table;
+  const SampleParams *sample;  // per output row; null when every row is greedy
 };
 
 template <typename T>
@@ -702,8 +722,12 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
   el.ldo = D.V;
   launch_gemm<T>(xn, D.d, e->ptr<T>(e->Ly.lm_head), n_out, D.V, D.d, 1, part, el, st);
   const int32_t *out_slot = prefill ? dm.seq_slot : dm.row_slot;
-  launch_argmax(logits, D.V, n_out, D.V, out_slot, e->ptr<int32_t>(e->Ly.slot_tok),
-                e->ptr<int32_t>(e->Ly.tok_log) + log_off, st);
+  if (dm.sample)
+    launch_sample(logits, D.V, n_out, D.V, dm.sample, out_slot, e->ptr<int32_t>(e->Ly.slot_tok),
+                  e->ptr<int32_t>(e->Ly.tok_log) + log_off, st);
+  else
+    launch_argmax(logits, D.V, n_out, D.V, out_slot, e->ptr<int32_t>(e->Ly.slot_tok),
+                  e->ptr<int32_t>(e->Ly.tok_log) + log_off, st);
   if (e->Ly.logits_log_bytes) {
     const size_t row_bytes = (size_t)D.V * 4;
     const size_t cap_rows = e->Ly.logits_log_bytes / row_bytes;
@@ -734,7 +758,23 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
   const size_t o_slot = region(M), o_pos = region(M), o_tok = region(M);
   const size_t o_ss = region(n_rows + 1), o_sq = region(n_rows), o_lm = region(n_rows);
   const size_t o_bt = region(block_table_host.size());
+  const size_t o_smp = region((size_t)n_rows * (sizeof(SampleParams) / 4));
   if (o * 4 > e->staging_bytes) return e->err = "step metadata overflow", LP_EINVAL;
+  // sampling parameters of the rows that emit a token; the draw's counter is
+  // (request id, index of the output token being produced)
+  bool any_sampling = false;
+  SampleParams *hs = (SampleParams *)(h + o_smp);
+  for (int j = 0; j < n_rows; ++j) {
+    const int ri = ps.reqs[j];
+    const SampleParams &sp = e->sampling[ri];
+    const int64_t id = e->reqs[ri].id;
+    const int k = ps.kind == 0 ? 0 : ps.pos[j] - e->reqs[ri].in_len + 1;
+    hs[j] = sp;
+    hs[j].counter[0] = (uint32_t)id;
+    hs[j].counter[1] = (uint32_t)((uint64_t)id >> 32);
+    hs[j].counter[2] = (uint32_t)k;
+    any_sampling |= sp.temperature > 0.f && sp.top_p > 0.f;
+  }
   int max_len = 0;
   if (ps.kind == 0) {
     int64_t row = 0;
@@ -767,7 +807,8 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
   }
   memcpy(h + o_bt, block_table_host.data(), block_table_host.size() * 4);
   HIPCHK(e, hipMemcpyAsync(d, h, o * 4, hipMemcpyHostToDevice, e->stream));
-  StepMeta dm{d + o_slot, d + o_pos, d + o_tok, d + o_ss, d + o_sq, d + o_lm, d + o_bt};
+  StepMeta dm{d + o_slot, d + o_pos, d + o_tok, d + o_ss, d + o_sq, d + o_lm, d + o_bt,
+              any_sampling ? (const SampleParams *)(d + o_smp) : nullptr};
   int rc;
   const bool pf = ps.kind == 0;
   int32_t *pool = e->ptr<int32_t>(e->Ly.pool), *stok = e->ptr<int32_t>(e->Ly.slot_tok);

@@ -107,6 +107,21 @@ void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, cons
 void launch_argmax(const float *logits, int64_t ld, int M, int V, const int32_t *out_slot,
                    int32_t *slot_tok, int32_t *tok_log, hipStream_t s);
 
+// Sampling parameters of one row: temperature (<= 0: greedy), top_k (0: off),
+// top_p (>= 1: off), and the Philox key / counter words of its random draw.
+struct SampleParams {
+  float temperature;
+  int32_t top_k;
+  float top_p;
+  uint32_t key[2];
+  uint32_t counter[3];
+};
+
+// Next token per row under its sampling parameters (see the kernel):
+// tok -> slot_tok[out_slot[m]] (when out_slot) and tok_out[m].
+void launch_sample(const float *logits, int64_t ld, int M, int V, const SampleParams *prm, const int32_t *out_slot,
+                   int32_t *slot_tok, int32_t *tok_out, hipStream_t s);
+
 // Weight generator: writes rows x cols values of canonical tensor `tensor_id`
 // to dst with row r stored at perm(r), in T.  `bf16_values`: round each value
 // to bf16 first (a bf16 model held in fp16 storage keeps its exact values).

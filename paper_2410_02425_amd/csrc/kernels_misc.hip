@@ -183,6 +183,212 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
   }
 }
 
+// ------------------------------------------------------------------ sampling
+
+// Non-greedy next-token choice per row (the sampling parameters carried by
+// requests, Sec. III-A).  Every decision after the per-token weights is exact
+// integer arithmetic, so the result does not depend on reduction order:
+//  * temperature <= 0 or top_p <= 0: greedy (lowest index among maxima);
+//  * candidates: all tokens, or with 0 < top_k < V those whose logit is at
+//    least the top_k-th largest logit (ties at it kept), found by a radix
+//    select over order-preserving integer keys of the logits;
+//  * weight of a candidate: q = floor(exp((logit - max) / T) * 2^40);
+//  * top_p < 1: with Z the candidates' total weight and
+//    need = ceil(Z * floor(top_p * 2^24) / 2^24), keep the candidates whose q
+//    is at least t, the largest value whose heavier-or-equal candidates sum to
+//    at least need (a radix descent over q with 64-bit mass histograms);
+//  * draw: u24 = the first Philox4x32-10 output word (key, counter as given)
+//    shifted right by 8; r = floor(Z_kept * u24 / 2^24); the token is the kept
+//    candidate, in vocabulary order, whose cumulative weight interval holds r.
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t b = __float_as_uint(x);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t q_weight(float l, float mx, float inv_t) {
+  const float w = __expf((l - mx) * inv_t);
+  return (uint64_t)(w * 1099511627776.0f);  // 2^40; w <= 1
+}
+
+// (a * b) >> 24 for a < 2^58, b < 2^25, rounded up when `up`
+__device__ __forceinline__ uint64_t mul_shift24(uint64_t a, uint64_t b, bool up) {
+  const uint64_t lo = a * b, hi = __umul64hi(a, b);
+  uint64_t r = (hi << 40) | (lo >> 24);
+  if (up && (lo & 0xFFFFFFull)) ++r;
+  return r;
+}
+
+__device__ uint64_t block_sum_u64(uint64_t v, uint64_t *red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t t = 0;
+  for (int w = 0; w < 16; ++w) t += red[w];
+  return t;
+}
+
+__global__ __launch_bounds__(1024) void sample_kernel(const float *__restrict__ logits, int64_t ld, int V,
+                                                      const SampleParams *__restrict__ prm, const int32_t *out_slot,
+                                                      int32_t *slot_tok, int32_t *tok_out) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  __shared__ uint64_t red[16];
+  __shared__ uint64_t hist[256];
+  __shared__ uint32_t cnt[256];
+  __shared__ uint64_t sel[4];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const float *row = logits + (int64_t)m * ld;
+  const SampleParams P = prm[m];
+  // 1. maximum (and the greedy answer)
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int c = tid; c < V; c += 1024) argmax_merge(best, bi, row[c], c);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) argmax_merge(best, bi, __shfl_xor(best, o, 64), __shfl_xor(bi, o, 64));
+  if ((tid & 63) == 0) {
+    sv[tid >> 6] = best;
+    si[tid >> 6] = bi;
+  }
+  __syncthreads();
+  for (int w = 0; w < 16; ++w) argmax_merge(best, bi, sv[w], si[w]);
+  int token = bi;
+  if (P.temperature > 0.f && P.top_p > 0.f && V > 1) {
+    const float mx = best, inv_t = 1.f / P.temperature;
+    // 2. top-k threshold on order keys: the top_k-th largest key
+    uint32_t kmin = 0;
+    if (P.top_k > 0 && P.top_k < V) {
+      uint32_t prefix = 0, above = 0;
+      for (int level = 0; level < 4; ++level) {
+        const int sh = 24 - 8 * level;
+        const uint32_t pmask = level ? (0xFFFFFFFFu << (32 - 8 * level)) : 0u;
+        for (int b = tid; b < 256; b += 1024) cnt[b] = 0;
+        __syncthreads();
+        for (int c = tid; c < V; c += 1024) {
+          const uint32_t k = order_key(row[c]);
+          if ((k & pmask) == prefix) atomicAdd(&cnt[(k >> sh) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          uint32_t acc = above;
+          int b = 255;
+          for (; b > 0; --b) {
+            if (acc + cnt[b] >= (uint32_t)P.top_k) break;
+            acc += cnt[b];
+          }
+          sel[0] = acc;
+          sel[1] = (uint64_t)b;
+        }
+        __syncthreads();
+        above = (uint32_t)sel[0];
+        prefix |= (uint32_t)sel[1] << sh;
+        __syncthreads();
+      }
+      kmin = prefix;
+    }
+    // 3. candidate weights and their total
+    uint64_t z = 0;
+    for (int c = tid; c < V; c += 1024) {
+      const float l = row[c];
+      if (order_key(l) >= kmin) z += q_weight(l, mx, inv_t);
+    }
+    z = block_sum_u64(z, red);
+    // 4. top-p threshold on weights
+    uint64_t tmin = 0, zk = z;
+    const uint32_t pfix = P.top_p >= 1.f ? (1u << 24) : max(1u, (uint32_t)(P.top_p * 16777216.0f));
+    if (pfix < (1u << 24)) {
+      const uint64_t need = mul_shift24(z, pfix, true);
+      uint64_t prefix = 0, above = 0;
+      for (int level = 0; level < 6; ++level) {
+        const int sh = 40 - 8 * level;
+        const uint64_t pmask = level ? (~0ull << (48 - 8 * level)) & 0xFFFFFFFFFFFFull : 0ull;
+        for (int b = tid; b < 256; b += 1024) hist[b] = 0;
+        __syncthreads();
+        for (int c = tid; c < V; c += 1024) {
+          const float l = row[c];
+          if (order_key(l) < kmin) continue;
+          const uint64_t q = q_weight(l, mx, inv_t);
+          if ((q & pmask) == prefix) atomicAdd((unsigned long long *)&hist[(q >> sh) & 255u], (unsigned long long)q);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          uint64_t acc = above;
+          int b = 255;
+          for (; b > 0; --b) {
+            if (acc + hist[b] >= need) break;
+            acc += hist[b];
+          }
+          sel[0] = acc;
+          sel[1] = (uint64_t)b;
+          sel[2] = acc + hist[b];
+        }
+        __syncthreads();
+        above = sel[0];
+        prefix |= sel[1] << sh;
+        zk = sel[2];
+        __syncthreads();
+      }
+      tmin = prefix;
+    }
+    // 5. draw: r in [0, zk), located by a scan over contiguous index chunks
+    uint32_t c4[4] = {P.counter[0], P.counter[1], P.counter[2], 0x53414D50u};
+    philox4x32_10(c4, P.key[0], P.key[1]);
+    const uint64_t r = mul_shift24(zk, c4[0] >> 8, false);
+    const int chunk = (V + 1023) / 1024;
+    const int c0 = tid * chunk, c1 = min(V, c0 + chunk);
+    uint64_t local = 0;
+    for (int c = c0; c < c1; ++c) {
+      const float l = row[c];
+      if (order_key(l) < kmin) continue;
+      const uint64_t q = q_weight(l, mx, inv_t);
+      if (q >= tmin) local += q;
+    }
+    // exclusive scan of the per-thread sums (thread order = index order)
+    uint64_t incl = local;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint64_t t = __shfl_up(incl, o, 64);
+      if ((tid & 63) >= o) incl += t;
+    }
+    __syncthreads();
+    if ((tid & 63) == 63) red[tid >> 6] = incl;
+    __syncthreads();
+    uint64_t base = 0;
+    for (int w = 0; w < (tid >> 6); ++w) base += red[w];
+    uint64_t pre = base + incl - local;
+    __shared__ int found;
+    if (tid == 0) found = bi;
+    __syncthreads();
+    if (local > 0 && r >= pre && r < pre + local) {
+      for (int c = c0; c < c1; ++c) {
+        const float l = row[c];
+        if (order_key(l) < kmin) continue;
+        const uint64_t q = q_weight(l, mx, inv_t);
+        if (q < tmin) continue;
+        if (r < pre + q) {
+          found = c;
+          break;
+        }
+        pre += q;
+      }
+    }
+    __syncthreads();
+    token = found;
+  }
+  if (tid == 0) {
+    if (out_slot) slot_tok[out_slot[m]] = token;
+    tok_out[m] = token;
+  }
+}
+
+void launch_sample(const float *logits, int64_t ld, int M, int V, const SampleParams *prm, const int32_t *out_slot,
+                   int32_t *slot_tok, int32_t *tok_out, hipStream_t s) {
+  if (M <= 0) return;
+  sample_kernel<<<M, 1024, 0, s>>>(logits, ld, V, prm, out_slot, slot_tok, tok_out);
+}
+
 template <typename T>
 __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t tid, int64_t rows,
                                    int64_t cols, float stdv, int perm, int hd, bool bf16_values) {

@@ -141,6 +141,14 @@ extern "C" int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t 
   return op_status();
 }
 
+extern "C" int lp_op_sample(const float *logits, int64_t ld, int32_t M, int32_t V, const lp_sample_params *params,
+                            int32_t *tokens, void *stream) {
+  OPCHK(logits && params && tokens && M >= 0 && V > 0 && ld >= V, "sample: args");
+  static_assert(sizeof(lp_sample_params) == sizeof(SampleParams), "sampling parameter layout");
+  launch_sample(logits, ld, M, V, (const SampleParams *)params, nullptr, nullptr, tokens, (hipStream_t)stream);
+  return op_status();
+}
+
 extern "C" int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_t tensor_id, int64_t rows,
                                  int64_t cols, float stdv, void *stream) {
   OPCHK(dst && rows > 0 && cols > 0 && tensor_id >= 0, "init_weight: args");

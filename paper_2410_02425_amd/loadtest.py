@@ -38,16 +38,21 @@ def _options(wl: synth.Workload, max_batch: int, max_batch_weight: int = 0, flag
 
 
 def characterize(eng: lp.Engine, wl: synth.Workload, vocab: int, users, requests_per_user: int = 2,
-                 min_requests: int = 4):
+                 min_requests: int = 4, sampling=None):
     """Closed-loop load test at each user count in ``users`` over the first
     max(requests_per_user * U, min_requests) requests of the workload's
-    seeded stream.  Returns one metrics dict per user count."""
+    seeded stream; ``sampling`` = (temperature, top_k, top_p) applies to
+    every request (seeded by its id), None keeps them greedy.  Returns one
+    metrics dict per user count."""
     rows = []
     for U in users:
         if U < 1 or U > eng.opt.max_batch:
             raise ValueError(f"user count {U} outside 1..max_batch ({eng.opt.max_batch})")
         reqs = synth.make_requests(wl, vocab, max(requests_per_user * U, min_requests))
         eng.submit(reqs)
+        if sampling is not None:
+            for r in reqs:
+                eng.set_sampling(r.id, *sampling, seed=1000 + r.id)
         eng.run(lp.LP_CLOSED_LOOP, U)
         rows.append({"users": U, **eng.latency_summary()})
     return rows
@@ -191,6 +196,7 @@ def main(argv=None):
     c.add_argument("--config", default="8b")
     c.add_argument("--users", default="1,2,4,8,16,32,64")
     c.add_argument("--requests-per-user", type=int, default=2)
+    c.add_argument("--sampling", default="", help="temperature,top_k,top_p for every request (default greedy)")
     b = sub.add_parser("batch-weight", help="search the maximum batch weight, then sweep budgets")
     b.add_argument("--config", default="8b")
     b.add_argument("--users", type=int, default=64)
@@ -235,8 +241,12 @@ def main(argv=None):
         users = [int(u) for u in args.users.split(",")]
         eng = lp.Engine(cfg, _options(wl, max(users)))
         eng.init_weights_random(key, 0.02)
-        for row in characterize(eng, wl, shape.vocab, users, args.requests_per_user):
-            print(json.dumps({"config": args.config, **row}), flush=True)
+        smp = None
+        if args.sampling:
+            t, k, p = args.sampling.split(",")
+            smp = (float(t), int(k), float(p))
+        for row in characterize(eng, wl, shape.vocab, users, args.requests_per_user, sampling=smp):
+            print(json.dumps({"config": args.config, "sampling": args.sampling or "greedy", **row}), flush=True)
         eng.close()
         return 0
     opt = _options(wl, args.users)

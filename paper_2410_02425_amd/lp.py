@@ -20,12 +20,12 @@ LP_FLAG_KEEP_LOGITS, LP_FLAG_TIME_KERNEL, LP_FLAG_BF16_ACTIVATIONS = 1, 2, 4
 
 EXPORTED = [
     "lp_arena_bytes_required", "lp_engine_create", "lp_load_weights", "lp_init_weights_random",
-    "lp_query_max_batch_weight", "lp_submit", "lp_set_forced_tokens", "lp_run", "lp_get_result",
+    "lp_query_max_batch_weight", "lp_submit", "lp_set_forced_tokens", "lp_set_sampling", "lp_run", "lp_get_result",
     "lp_get_token_times", "lp_get_run_stats", "lp_get_step_log", "lp_get_logits", "lp_last_error",
     "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
     "lp_wg_fit", "lp_wg_info", "lp_wg_bins", "lp_wg_sample", "lp_wg_sample_independent", "lp_wg_free",
     "lp_op_gemm", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
-    "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight",
+    "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight", "lp_op_sample",
 ]
 
 
@@ -62,6 +62,11 @@ class RunStats(C.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+class SampleParams(C.Structure):
+    _fields_ = [("temperature", C.c_float), ("top_k", C.c_int32), ("top_p", C.c_float),
+                ("key", C.c_uint32 * 2), ("counter", C.c_uint32 * 3)]
+
+
 class LatencySummary(C.Structure):
     _fields_ = [("n_requests", C.c_int64), ("output_tokens", C.c_int64), ("itl_count", C.c_int64),
                 ("ttft_p50_ns", C.c_double), ("nttft_p50_ns", C.c_double), ("itl_p50_ns", C.c_double),
@@ -92,6 +97,7 @@ def lib():
             "lp_query_max_batch_weight": [vp, P(i64)],
             "lp_submit": [vp, P(Request), i32],
             "lp_set_forced_tokens": [vp, i64, P(i32), i32],
+            "lp_set_sampling": [vp, i64, f32, i32, f32, C.c_uint64],
             "lp_run": [vp, i32, i32],
             "lp_get_result": [vp, i64, P(i32), P(i64), P(i64), P(i64), P(i64)],
             "lp_get_token_times": [vp, i64, P(i64)],
@@ -115,6 +121,7 @@ def lib():
             "lp_op_prefill_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp],
             "lp_op_argmax": [vp, i64, i32, i32, vp, vp],
             "lp_op_init_weight": [i32, vp, C.c_uint64, i32, i64, i64, f32, vp],
+            "lp_op_sample": [vp, i64, i32, i32, vp, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -235,6 +242,10 @@ class Engine:
                                    itl.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(e2e), C.byref(arr)), self.h)
         return {"tokens": toks, "ttft_ns": ttft.value, "itl_ns": itl[: r.out_len - 1], "e2e_ns": e2e.value,
                 "arrival_ns": arr.value}
+
+    def set_sampling(self, rid: int, temperature: float, top_k: int = 0, top_p: float = 1.0, seed: int = 0):
+        """Sampling parameters of submitted request rid (greedy until set)."""
+        _check(lib().lp_set_sampling(self.h, rid, temperature, top_k, top_p, seed & 0xFFFFFFFFFFFFFFFF), self.h)
 
     def latency_summary(self) -> dict:
         """Load-test metrics of the last run over all submitted requests."""
@@ -431,6 +442,21 @@ def op_prefill_attention(q, out, kc, vc, block_table, seq_start, seq_slot, max_l
 def op_argmax(logits, tokens):
     M, V = logits.shape
     _check(lib().lp_op_argmax(_ptr(logits), logits.stride(0), M, V, _ptr(tokens), _stream()))
+
+
+def op_sample(logits, params, tokens):
+    """params: a device tensor holding M SampleParams records (uint8 view)."""
+    M, V = logits.shape
+    _check(lib().lp_op_sample(_ptr(logits), logits.stride(0), M, V, _ptr(params), _ptr(tokens), _stream()))
+
+
+def sample_params_array(rows) -> np.ndarray:
+    """Packs (temperature, top_k, top_p, (k0, k1), (c0, c1, c2)) tuples into
+    the byte layout of lp_sample_params."""
+    arr = (SampleParams * len(rows))()
+    for i, (t, k, p, key, ctr) in enumerate(rows):
+        arr[i] = SampleParams(t, k, p, (C.c_uint32 * 2)(*key), (C.c_uint32 * 3)(*ctr))
+    return np.frombuffer(bytes(arr), dtype=np.uint8).copy()
 
 
 def op_init_weight(dst, seed, tensor_id, std):

@@ -1,0 +1,168 @@
+"""Next-token sampling (temperature, top-k, top-p): oracle pins from the
+definitions, then the kernel against the oracle.  The kernel's weights come
+from float32 exp, the oracle's from float64, so a token may differ only where
+the draw falls within a hair of an interval boundary or a weight ties with
+the nucleus threshold; everything else must match exactly."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import sampling as SP
+from paper_2410_02425_amd import lp, synth
+
+
+# ------------------------------------------------------------------ oracle pins
+
+def test_greedy_cases():
+    l = [0.5, 2.0, 2.0, -1.0]
+    assert SP.choose(l, 0.0, 0, 1.0, 12345)[0] == 1      # temperature 0
+    assert SP.choose(l, 1.0, 0, 0.0, 12345)[0] == 1      # top_p 0
+    assert SP.choose([3.0], 1.0, 0, 1.0, 777)[0] == 0    # one token
+
+
+def test_top_k_keeps_ties_at_the_threshold():
+    l = [1.0, 3.0, 3.0, 2.0]
+    cand, _ = SP.weights(l, 1.0, 2)
+    assert cand == [False, True, True, False]
+    cand, _ = SP.weights(l, 1.0, 3)
+    assert cand == [False, True, True, True]
+    cand, _ = SP.weights(l, 1.0, 1)
+    assert cand == [False, True, True, False]          # the largest value repeats
+    for u in range(0, 1 << 24, 1 << 20):
+        assert SP.choose([0.0, 5.0, 1.0], 0.7, 1, 1.0, u)[0] == 1
+
+
+def test_nucleus_smallest_heavy_set():
+    # weights proportional to 0.5, 0.3, 0.15, 0.05 (logits are their logs)
+    l = [math.log(x) for x in (0.15, 0.5, 0.05, 0.3)]
+    cand, q = SP.weights(l, 1.0, 0)
+    keep, zk, t = SP.nucleus(cand, q, 0.7)
+    assert keep == [False, True, False, True]           # 0.5 alone < 0.7 <= 0.5 + 0.3
+    keep, _, _ = SP.nucleus(cand, q, 0.45)
+    assert keep == [False, True, False, False]
+    keep, _, _ = SP.nucleus(cand, q, 0.96)
+    assert keep == [True, True, True, True]             # 0.95 < 0.96
+    keep, _, _ = SP.nucleus(cand, q, 1.0)
+    assert keep == cand
+
+
+def test_draw_proportions_are_exact():
+    """Over a stratified grid of u24 values, each token is drawn in proportion
+    to its weight, to within one grid step."""
+    l = [0.3, -0.2, 1.1, 0.0, 0.7]
+    T = 0.8
+    cand, q = SP.weights(l, T, 0)
+    zk = sum(q)
+    n = 1 << 12
+    counts = np.zeros(len(l), dtype=np.int64)
+    for k in range(n):
+        counts[SP.choose(l, T, 0, 1.0, k << 12)[0]] += 1
+    exact = np.array(q, dtype=np.float64) / zk * n
+    assert np.all(np.abs(counts - exact) <= 1.0)
+    # and the weights are the softmax of logits / T
+    p = np.exp((np.array(l) - max(l)) / T)
+    np.testing.assert_allclose(np.array(q) / zk, p / p.sum(), rtol=1e-9)
+
+
+def test_draw_u24_uses_the_philox_kat_generator():
+    # the draw is the published Philox4x32-10: compare with the generator that
+    # the known-answer test pins
+    key, ctr = (0x243F6A88, 0x85A308D3), (5, 0, 3)
+    w = synth.philox4x32_10(5, 0, 3, SP.PHILOX_WORD3, *key)[0]
+    assert SP.draw_u24(key, ctr) == int(np.asarray(w).reshape(-1)[0]) >> 8
+    assert 0 <= SP.draw_u24(key, ctr) < (1 << 24)
+
+
+# ------------------------------------------------------------------ kernel vs oracle
+
+def check(logits, t, k, p, u24, got):
+    """'exact' if got is the oracle's token; 'edge' if it differs only where
+    float32 and float64 weights can disagree; raises otherwise."""
+    want, info = SP.choose(logits, t, k, p, u24)
+    if got == want:
+        return "exact"
+    assert info is not None, (got, want)
+    keep, q, zk, r = info
+    tol = 1e-5
+    # the kernel's token must be a candidate with a weight near the kept set
+    cand, _ = SP.weights(logits, t, k)
+    assert cand[got], (got, want)
+    kept_min = min(qq for qq, kk in zip(q, keep) if kk)
+    assert q[got] >= kept_min * (1 - tol), (got, want)
+    # ... and adjacent (in index order among weights near the kept set) to the
+    # oracle's interval boundary that r sits next to
+    start = sum(qq for i, (qq, kk) in enumerate(zip(q, keep)) if kk and i < want)
+    near = min(abs(r - start), abs(r - (start + q[want])))
+    assert near <= tol * zk or abs(q[got] - kept_min) <= tol * kept_min, (got, want, near / zk)
+    return "edge"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("V", [1000, 128256])
+def test_sample_kernel_matches_oracle(V):
+    import torch
+    torch.cuda.set_device(0)
+    rng = np.random.default_rng(V)
+    rows, logits = [], []
+    combos = [(t, k, p) for t in (0.0, 0.5, 1.0, 1.7) for k in (0, 1, 7, 50) for p in (1.0, 0.9, 0.5, 0.05)]
+    for i, (t, k, p) in enumerate(combos):
+        scale = (0.3, 2.0, 6.0)[i % 3]
+        l = (rng.standard_normal(V) * scale).astype(np.float32)
+        if i % 5 == 0:
+            l[rng.integers(0, V, 20)] = l.max()          # repeated maxima
+        if i % 7 == 0:
+            l = np.round(l, 1).astype(np.float32)       # many ties
+        logits.append(l)
+        key = (int(rng.integers(0, 2**32)), int(rng.integers(0, 2**32)))
+        ctr = (i, 0, int(rng.integers(0, 1000)))
+        rows.append((t, k, p, key, ctr))
+    L = torch.tensor(np.stack(logits), device="cuda")
+    prm = torch.tensor(lp.sample_params_array(rows), device="cuda")
+    tok = torch.full((len(rows),), -1, dtype=torch.int32, device="cuda")
+    lp.op_sample(L, prm, tok)
+    torch.cuda.synchronize()
+    got = tok.cpu().numpy()
+    kinds = []
+    for i, (t, k, p, key, ctr) in enumerate(rows):
+        kinds.append(check(logits[i].astype(np.float64), t, k, p, SP.draw_u24(key, ctr), int(got[i])))
+        if i % 16 == 15:
+            print(f"V={V}: {i + 1} rows checked", flush=True)
+    print(f"V={V}: {kinds.count('exact')} exact, {kinds.count('edge')} boundary of {len(kinds)}")
+    assert kinds.count("exact") >= len(kinds) - 2
+
+
+@pytest.mark.gpu
+def test_engine_draws_with_each_requests_parameters():
+    """Every token the engine emits is the sampler's choice on the logits that
+    produced it, with the request's parameters and the draw keyed by (seed,
+    request id, output index); greedy requests stay greedy; runs repeat."""
+    import torch
+    torch.cuda.set_device(0)
+    shape = synth.SHAPES["tiny"]
+    eng = lp.Engine(lp.make_config(shape), lp.EngineOptions(4, 96, 0, 4096, 0, lp.LP_FLAG_KEEP_LOGITS))
+    eng.init_weights_random(9, 0.05)
+    rng = np.random.default_rng(1)
+    reqs = [synth.Request(10 + i, rng.integers(0, shape.vocab, size=n).astype(np.int32), o)
+            for i, (n, o) in enumerate([(20, 12), (5, 9), (33, 10), (1, 8), (12, 11)])]
+    params = {10: (1.0, 0, 1.0, 111), 11: (0.7, 20, 1.0, 222), 12: (1.3, 0, 0.5, 333), 14: (0.9, 5, 0.8, 2**40 + 5)}
+    eng.submit(reqs)
+    for rid, (t, k, p, seed) in params.items():
+        eng.set_sampling(rid, t, k, p, seed)
+    eng.run(lp.LP_CLOSED_LOOP, 3)
+    first = {r.id: eng.result(r.id)["tokens"].copy() for r in reqs}
+    kinds = []
+    for r in reqs:
+        t, k, p, seed = params.get(r.id, (0.0, 0, 1.0, 0))
+        key = (seed & 0xFFFFFFFF, seed >> 32)
+        for j in range(r.out_len):
+            logits = eng.logits(r.id, j).astype(np.float64)
+            u24 = SP.draw_u24(key, (r.id & 0xFFFFFFFF, r.id >> 32, j))
+            kinds.append(check(logits, t, k, p, u24, int(first[r.id][j])))
+    assert kinds.count("exact") >= len(kinds) - 1
+    # sampled requests do not simply follow the argmax
+    assert any(int(first[10][j]) != int(np.argmax(eng.logits(10, j))) for j in range(12))
+    eng.run(lp.LP_CLOSED_LOOP, 3)
+    for r in reqs:
+        assert np.array_equal(eng.result(r.id)["tokens"], first[r.id])
+    eng.close()
