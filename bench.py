@@ -111,17 +111,18 @@ def copy_bandwidth_gbs(torch, reps: int = 10) -> float:
 def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.0):
     """The oracle, unchanged, on a bounded sample of the workload: one request
     (its prompt taken from the workload, length near the mean) generated at
-    depth 1 and 2 with full-width weights, extrapolated linearly in depth to
-    the full model.  The number of output tokens is sized from a 2-token probe
-    so that the two timed runs take about budget_s.  Returns the oracle's
-    output tokens/s at full depth for that request."""
+    depth 1 and 4 with full-width weights, extrapolated linearly in depth to
+    the full model (three layers of difference keep timing noise small).  The
+    number of output tokens is sized from short probes so that the two timed
+    runs take about budget_s.  Returns the oracle's output tokens/s at full
+    depth for that request."""
     from oracle import transformer as T
 
     r = sorted(reqs, key=lambda q: abs(q.in_len - 553))[0]
     lm_rows = None
     embed_rows = None
     models = {}
-    for depth in (1, 2):
+    for depth in (1, 4):
         sh = shape.with_layers(depth)
         w = {}
         used = np.unique(r.prompt)
@@ -142,21 +143,21 @@ def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.
         cfg = dict(n_layers=depth, d_model=sh.d_model, n_heads=sh.n_heads, n_kv_heads=sh.n_kv_heads,
                    ffn_dim=sh.ffn_dim, vocab=sh.vocab, rope_theta=sh.rope_theta, norm_eps=sh.norm_eps)
         models[depth] = T.Model(cfg, w)
-    # probes at depth 2: prefill alone (1 token) and prefill + 3 decode tokens;
+    # probes at depth 4: prefill alone (1 token) and prefill + 3 decode tokens;
     # size the sample so that both timed runs together take about budget_s
     t0 = time.perf_counter()
-    T.generate(models[2], r.prompt, 1)
+    T.generate(models[4], r.prompt, 1)
     t_pre = time.perf_counter() - t0
     t0 = time.perf_counter()
-    T.generate(models[2], r.prompt, 4)
+    T.generate(models[4], r.prompt, 4)
     per_tok = max((time.perf_counter() - t0 - t_pre) / 3, 1e-4)
-    n_out = int(min(max(6, (budget_s - 2 * t_pre) / (1.75 * per_tok)), 1024))
+    n_out = int(min(max(6, (budget_s - 1.4 * t_pre) / (1.4 * per_tok)), 1024))
     times = {}
-    for depth in (1, 2):
+    for depth in (1, 4):
         t0 = time.perf_counter()
         T.generate(models[depth], r.prompt, n_out)
         times[depth] = time.perf_counter() - t0
-    per_layer = max(times[2] - times[1], 1e-9)
+    per_layer = max((times[4] - times[1]) / 3, 1e-9)
     fixed = max(times[1] - per_layer, 0.0)
     full = fixed + per_layer * shape.n_layers
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
@@ -166,7 +167,7 @@ def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.
         "cores": cores,
         "kind": "oracle",
         "sample": (f"one 8B-shape request (in_len {r.in_len}, {n_out} output tokens), float64 oracle with "
-                   f"full-width weights at depth 1 ({times[1]:.1f} s) and 2 ({times[2]:.1f} s), extrapolated "
+                   f"full-width weights at depth 1 ({times[1]:.1f} s) and 4 ({times[4]:.1f} s), extrapolated "
                    f"linearly to {shape.n_layers} layers"),
     }
 

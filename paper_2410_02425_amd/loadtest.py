@@ -204,6 +204,9 @@ def main(argv=None):
     b.add_argument("--weights", default="8192,16384,32768,65536,131072,max",
                    help="budgets in tokens; 'max' is the searched maximum")
     b.add_argument("--arena-gb", type=float, default=0.0, help="memory budget (default: 85%% of free HBM)")
+    o = sub.add_parser("open", help="open-loop run of a Poisson-arrival workload (e.g. 8b-poisson)")
+    o.add_argument("--config", default="8b-poisson")
+    o.add_argument("--requests", type=int, default=0, help="first N requests of the workload (default: all)")
     g = sub.add_parser("generator", help="joint vs independent request parameters (workload generator)")
     g.add_argument("--config", default="8b")
     g.add_argument("--users", default="4,16,64")
@@ -213,9 +216,25 @@ def main(argv=None):
 
     import torch
     torch.cuda.set_device(0)
-    shape, wl = synth.SHAPES[args.config], synth.WORKLOADS[args.config]
+    wl = synth.WORKLOADS[args.config]
+    shape = synth.SHAPES[args.config.split("-")[0]]
     cfg = lp.make_config(shape)
     key = synth.workload_seeds(wl.base_seed)[0]
+    if args.cmd == "open":
+        reqs = synth.make_requests(wl, shape.vocab, args.requests or None)
+        eng = lp.Engine(cfg, _options(wl, wl.max_batch))
+        eng.init_weights_random(key, 0.02)
+        eng.submit(reqs)
+        eng.run(lp.LP_OPEN_LOOP, wl.max_batch)
+        log = eng.step_log()
+        dec = [st for st in log if st["kind"] == "decode"]
+        print(json.dumps({"config": args.config, "rate_per_s": wl.rate_per_s, "max_batch": wl.max_batch,
+                          "arrival_span_s": reqs[-1].arrival_ns / 1e9, "decode_steps": len(dec),
+                          "mean_decode_rows": float(np.mean([st["n_rows"] for st in dec])) if dec else 0.0,
+                          "max_decode_rows": max((st["n_rows"] for st in dec), default=0),
+                          **eng.latency_summary()}), flush=True)
+        eng.close()
+        return 0
     if args.cmd == "generator":
         import time
         recs = synth.trace_records(wl.base_seed, args.trace_records)
