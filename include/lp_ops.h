@@ -43,7 +43,9 @@ int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t n_part, co
  * one layer in blocks of 64 tokens: k_cache [n_blocks][Hkv][64][hd],
  * v_cache [n_blocks][Hkv][hd][64] (transposed per block); block_table
  * [*][max_blocks] int32 lists each slot's blocks.  Row m reads slot
- * row_slot[m] over positions 0..row_pos[m] (ctx = row_pos[m] + 1 <= max_ctx).
+ * row_slot[m] over positions 0..row_pos[m] (ctx = row_pos[m] + 1 <= max_ctx;
+ * a larger ctx is clamped to max_ctx, so the kernels stay inside ws and the
+ * first max_ctx positions of the block table).
  * ws: at least lp_op_decode_attention_ws_bytes(M, Hq, hd, max_ctx) bytes. */
 size_t lp_op_decode_attention_ws_bytes(int32_t M, int32_t n_heads, int32_t head_dim, int32_t max_ctx);
 int lp_op_decode_attention(int32_t dtype, const void *q, void *out, const void *k_cache, const void *v_cache,

@@ -3,7 +3,9 @@
 // Decode: each request row attends to its whole cached context.  The context
 // is cut into chunks of DEC_CHUNK positions; one workgroup handles one (row,
 // kv head, chunk) and all query heads of that kv head's group, four waves each
-// taking one 64-position KV block.  Partial (max, sum, unnormalised output)
+// taking one 64-position KV block.  The grid holds only live chunks: work
+// item i is the i-th (row, chunk) pair in row-major order, found by a prefix
+// sum over the rows' chunk counts.  Partial (max, sum, unnormalised output)
 // triples are merged by a combine pass (log-sum-exp rescaling).
 //
 // Prefill: causal attention of packed prompt rows, one workgroup per 64 query
@@ -20,6 +22,46 @@ constexpr int MAX_GROUP = 8;    // query heads per kv head
 size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx) {
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
   return (size_t)M * n_heads * splits * (head_dim + 2) * sizeof(float);
+}
+
+int decode_attention_chunks(int ctx) { return (ctx + DEC_CHUNK - 1) / DEC_CHUNK; }
+
+// Work item -> (row m, chunk s, slot, context) of a decode workgroup.  Item i
+// is the i-th pair in the row-major list of every row's chunks (a row of
+// context c has ceil(c / DEC_CHUNK)); contexts are clamped to max_ctx.  Each
+// wave computes it on its own: lane l reads row base + l, an inclusive scan
+// over the 64 lanes gives the chunks up to that row, and the first lane whose
+// running count exceeds the item is the row.  False past the last item.
+struct DecodeItem {
+  int m, s, slot, ctx;
+};
+__device__ __forceinline__ bool decode_item(const RowMeta &rows, int M, int max_ctx, int item, DecodeItem &it) {
+  const int lane = threadIdx.x & 63;
+  int before = 0;
+  for (int base = 0; base < M; base += 64) {
+    const int r = base + lane;
+    const int ctx = r < M ? min(rows.row_pos[r] + 1, max_ctx) : 0;
+    const int slot = r < M ? rows.row_slot[r] : 0;
+    const int n = ctx > 0 ? (ctx + DEC_CHUNK - 1) / DEC_CHUNK : 0;
+    int incl = n;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    const int total = __shfl(incl, 63, 64);
+    const int rel = item - before;
+    if (rel < total) {
+      const int k = __popcll(__ballot(incl <= rel));  // rows wholly before the item
+      it.m = base + k;
+      it.s = rel - __shfl(incl - n, k, 64);
+      it.slot = __shfl(slot, k, 64);
+      it.ctx = __shfl(ctx, k, 64);
+      return true;
+    }
+    before += total;
+  }
+  return false;
 }
 
 template <typename T>
@@ -56,21 +98,19 @@ struct Vec8<float> {
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const T *__restrict__ q, RowMeta rows,
                                                           KVCache kv, int layer, int M, int n_heads,
-                                                          int max_splits, float *__restrict__ ws) {
+                                                          int max_ctx, int max_splits, float *__restrict__ ws) {
   constexpr int DPL = HD / 64;  // dims per lane in P.V
   __shared__ float qs[G][HD];
   __shared__ float ps[4][G][64];
   __shared__ float wm[4][G], wl[4][G];
   __shared__ float wo[4][G][HD];
-  // one linear grid, KV head fastest and chunk slowest: the live chunks of
-  // short contexts are the low block ids, which the dispatcher spreads evenly
-  // over the XCDs, and the idle ones (past a row's context) come last
-  const int g = blockIdx.x % kv.n_kv_heads, m = (blockIdx.x / kv.n_kv_heads) % M;
-  const int s = blockIdx.x / (kv.n_kv_heads * M);
+  // KV head fastest: consecutive block ids, which the dispatcher deals out
+  // round-robin over the XCDs, are the heads of one work item
+  const int g = blockIdx.x % kv.n_kv_heads;
+  DecodeItem it;
+  if (!decode_item(rows, M, max_ctx, blockIdx.x / kv.n_kv_heads, it)) return;
+  const int m = it.m, s = it.s, slot = it.slot, ctx = it.ctx;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int slot = rows.row_slot[m];
-  const int ctx = rows.row_pos[m] + 1;
-  if (s * DEC_CHUNK >= ctx) return;
 
   for (int e = threadIdx.x; e < G * HD; e += 256)
     qs[e / HD][e % HD] = Act<T>::ld(q[((int64_t)m * n_heads + g * G) * HD + e]);
@@ -166,22 +206,44 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T *__restrict__ 
   }
 }
 
+// Merges a row's chunk partials for one query head: out = sum_s e^(m_s - M) o_s
+// / sum_s e^(m_s - M) l_s with M the largest chunk maximum, taken in one pass
+// with a running maximum; each thread owns one output dimension and issues
+// the loads of eight chunks before it uses any.
 template <typename T, int HD>
-__global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_heads, int max_splits,
-                                                            const float *__restrict__ ws,
+__global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_heads, int max_ctx,
+                                                            int max_splits, const float *__restrict__ ws,
                                                             T *__restrict__ out) {
+  constexpr int U = 8;
   const int h = blockIdx.x, m = blockIdx.y;
   const int c = threadIdx.x;
-  const int ctx = rows.row_pos[m] + 1;
-  const int ns = (ctx + DEC_CHUNK - 1) / DEC_CHUNK;
+  const int ctx = min(rows.row_pos[m] + 1, max_ctx);
+  const int ns = ctx > 0 ? (ctx + DEC_CHUNK - 1) / DEC_CHUNK : 0;
   const float *src = ws + ((int64_t)m * n_heads + h) * max_splits * (HD + 2);
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, src[s * (HD + 2) + HD]);
-  float num = 0.f, den = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float f = __expf(src[s * (HD + 2) + HD] - M);
-    num += f * src[s * (HD + 2) + c];
-    den += f * src[s * (HD + 2) + HD + 1];
+  float M = -INFINITY, num = 0.f, den = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += U) {
+    float mv[U], ov[U], lv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float *p = src + (int64_t)min(s0 + u, ns - 1) * (HD + 2);
+      mv[u] = p[HD];
+      ov[u] = p[c];
+      lv[u] = p[HD + 1];
+    }
+    float nm = M;
+#pragma unroll
+    for (int u = 0; u < U; ++u) nm = fmaxf(nm, mv[u]);
+    if (nm == -INFINITY) continue;
+    const float r = __expf(M - nm);  // 0 while M is still -inf
+    num *= r;
+    den *= r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float f = (s0 + u < ns) ? __expf(mv[u] - nm) : 0.f;
+      num += f * ov[u];
+      den += f * lv[u];
+    }
+    M = nm;
   }
   out[((int64_t)m * n_heads + h) * HD + c] = Act<T>::st(num / den);
 }
@@ -195,24 +257,22 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
 // of the block are requested before any is used.
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restrict__ q, RowMeta rows, KVCache kv,
-                                                               int layer, int M, int n_heads, int max_splits,
-                                                               float *__restrict__ ws) {
+                                                               int layer, int M, int n_heads, int max_ctx,
+                                                               int max_splits, float *__restrict__ ws) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int KS = HD / 32;  // contraction steps over head_dim
   constexpr int NT = HD / 16;  // 16-wide output tiles over head_dim
   __shared__ T pls[4][16][64 + 8];
   __shared__ float wm[4][16], wl[4][16];
   __shared__ float wo[4][G][HD];
-  // one linear grid, KV head fastest and chunk slowest: the live chunks of
-  // short contexts are the low block ids, which the dispatcher spreads evenly
-  // over the XCDs, and the idle ones (past a row's context) come last
-  const int g = blockIdx.x % kv.n_kv_heads, m = (blockIdx.x / kv.n_kv_heads) % M;
-  const int s = blockIdx.x / (kv.n_kv_heads * M);
+  // KV head fastest: consecutive block ids, which the dispatcher deals out
+  // round-robin over the XCDs, are the heads of one work item
+  const int g = blockIdx.x % kv.n_kv_heads;
+  DecodeItem it;
+  if (!decode_item(rows, M, max_ctx, blockIdx.x / kv.n_kv_heads, it)) return;
+  const int m = it.m, s = it.s, slot = it.slot, ctx = it.ctx;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, quad = lane >> 4, kq = quad * 8;
-  const int slot = rows.row_slot[m];
-  const int ctx = rows.row_pos[m] + 1;
-  if (s * DEC_CHUNK >= ctx) return;
   const int blk_pos = s * DEC_CHUNK + wave * 64;
   const int nvalid = max(0, min(64, ctx - blk_pos));
 
@@ -334,37 +394,38 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 
 template <typename T, int HD, int G>
 static void launch_decode_group(dim3 grid, const T *q, const RowMeta &rows, const KVCache &kv, int layer, int M,
-                                int n_heads, int splits, float *ws, hipStream_t s) {
+                                int n_heads, int max_ctx, int splits, float *ws, hipStream_t s) {
   if constexpr (sizeof(T) == 2)
-    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, splits, ws);
+    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits, ws);
   else
-    decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, splits, ws);
+    decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits, ws);
 }
 
 template <typename T, int HD>
 static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s) {
   const int G = n_heads / kv.n_kv_heads;
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
-  dim3 grid((unsigned)(splits * kv.n_kv_heads * M));
+  if (items <= 0 || items > M * splits) items = M * splits;
+  dim3 grid((unsigned)(items * kv.n_kv_heads));
   switch (G) {
-    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
-    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
-    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
-    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, M, n_heads, splits, ws, s); break;
+    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
+    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
+    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
+    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
     default: return;
   }
-  decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, splits, ws, out);
+  decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, max_ctx, splits, ws, out);
 }
 
 template <typename T>
 void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s) {
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s) {
   if (M <= 0) return;
   if (kv.head_dim == 128)
-    launch_decode_hd<T, 128>(q, out, rows, kv, layer, M, n_heads, max_ctx, ws, s);
+    launch_decode_hd<T, 128>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s);
   else if (kv.head_dim == 64)
-    launch_decode_hd<T, 64>(q, out, rows, kv, layer, M, n_heads, max_ctx, ws, s);
+    launch_decode_hd<T, 64>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s);
 }
 
 // ------------------------------------------------------------------ prefill
@@ -612,7 +673,7 @@ void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, cons
 
 #define INST(T)                                                                                     \
   template void launch_decode_attention<T>(const T *, T *, const RowMeta &, const KVCache &, int,   \
-                                           int, int, int, float *, hipStream_t);                    \
+                                           int, int, int, int, float *, hipStream_t);               \
   template void launch_prefill_attention<T>(const T *, T *, const int32_t *, const int32_t *, int, \
                                             int, const KVCache &, int, int, hipStream_t);
 INST(float)

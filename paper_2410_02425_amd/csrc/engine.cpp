@@ -638,8 +638,8 @@ KVCache kv_of(lp_engine *e, const int32_t *block_table) {
 // prefill: n_seq sequences described by seq_start/seq_slot, LM head over
 // lm_rows; decode: rows attend to their slots' caches.
 template <typename T>
-int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_len, const StepMeta &dm,
-               int64_t log_off, int64_t step) {
+int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_len, int attn_items,
+               const StepMeta &dm, int64_t log_off, int64_t step) {
   const int step_ring = (int)(step % RING);
   // LP_FLAG_TIME_KERNEL: one layer's gate/up launch per decode step, rotating
   // over the layers, carries two events bound to its dispatch
@@ -682,7 +682,8 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
     if (prefill)
       launch_prefill_attention<T>(qb, ab, dm.seq_start, dm.seq_slot, n_seq, max_len, kv, l, D.Hq, st);
     else
-      launch_decode_attention<T>(qb, ab, rows, kv, l, M, D.Hq, max_len, e->ptr<float>(e->Ly.attn_ws), st);
+      launch_decode_attention<T>(qb, ab, rows, kv, l, M, D.Hq, max_len, attn_items, e->ptr<float>(e->Ly.attn_ws),
+                                 st);
     Epi eo{};
     eo.kind = EPI_RESID;
     eo.out = x;
@@ -775,7 +776,7 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
     hs[j].counter[2] = (uint32_t)k;
     any_sampling |= sp.temperature > 0.f && sp.top_p > 0.f;
   }
-  int max_len = 0;
+  int max_len = 0, attn_items = 0;
   if (ps.kind == 0) {
     int64_t row = 0;
     for (int j = 0; j < n_rows; ++j) {
@@ -799,6 +800,7 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
       h[o_slot + j] = ps.slots[j];
       h[o_pos + j] = ps.pos[j];
       max_len = std::max(max_len, ps.pos[j] + 1);  // decode: the longest context
+      attn_items += decode_attention_chunks(ps.pos[j] + 1);
       // the token fed at position pos is output token number pos - in_len
       const int k = ps.pos[j] - q.in_len;
       const bool forced = e->forced_off[ri] >= 0 && k < e->forced_n[ri];
@@ -816,16 +818,16 @@ static int launch_step(lp_engine *e, const PlanStep &ps, int64_t step, int64_t l
   switch (e->D.act) {
     case ACT_F16:
       launch_embed<f16_t>(e->ptr<f16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
-      rc = run_layers<f16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
+      rc = run_layers<f16_t>(e, pf, M, n_rows, n_rows, max_len, attn_items, dm, log_off, step);
       break;
     case ACT_BF16:
       launch_embed<bf16_t>(e->ptr<bf16_t>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d,
                            e->stream);
-      rc = run_layers<bf16_t>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
+      rc = run_layers<bf16_t>(e, pf, M, n_rows, n_rows, max_len, attn_items, dm, log_off, step);
       break;
     default:
       launch_embed<float>(e->ptr<float>(e->Ly.embed), pool, dm.row_tok, dm.row_slot, stok, x, M, e->D.d, e->stream);
-      rc = run_layers<float>(e, pf, M, n_rows, n_rows, max_len, dm, log_off, step);
+      rc = run_layers<float>(e, pf, M, n_rows, n_rows, max_len, attn_items, dm, log_off, step);
   }
   if (rc) return rc;
   HIPCHK(e, hipEventRecord(e->ev_step[ring], e->stream));

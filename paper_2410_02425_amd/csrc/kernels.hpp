@@ -87,13 +87,17 @@ int prefill_gemm_splits(int M, int N, int K);
 template <typename T>
 void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s);
 
-// Decode attention: row m attends to ctx = row_pos[m] + 1 cached positions of
-// its slot.  q [M][Hq][hd], out [M][Hq][hd] (activation type).  Uses
-// workspace `ws` (see decode_attention_ws_bytes).
+// Decode attention: row m attends to ctx = min(row_pos[m] + 1, max_ctx)
+// cached positions of its slot.  q [M][Hq][hd], out [M][Hq][hd] (activation
+// type).  Uses workspace `ws` (see decode_attention_ws_bytes).  `items` is the
+// rows' total chunk count, the sum of decode_attention_chunks(ctx) over the
+// rows, which sizes the grid to the live work; 0 launches the upper bound
+// M * decode_attention_chunks(max_ctx), whose surplus workgroups exit.
 size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx);
+int decode_attention_chunks(int ctx);
 template <typename T>
 void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, float *ws, hipStream_t s);
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s);
 
 // Prefill (causal) attention over packed sequences: sequence j covers rows
 // [seq_start[j], seq_start[j+1]) at positions 0.., KV slot seq_slot[j].

@@ -100,14 +100,14 @@ extern "C" int lp_op_decode_attention(int32_t dtype, const void *q, void *out, c
   RowMeta rows{row_slot, row_pos};
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
-    launch_decode_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, rows, kv, 0, M, n_heads, max_ctx,
+    launch_decode_attention<bf16_t>((const bf16_t *)q, (bf16_t *)out, rows, kv, 0, M, n_heads, max_ctx, 0,
                                     (float *)ws, s);
   else if (dtype == LP_F16)
-    launch_decode_attention<f16_t>((const f16_t *)q, (f16_t *)out, rows, kv, 0, M, n_heads, max_ctx,
+    launch_decode_attention<f16_t>((const f16_t *)q, (f16_t *)out, rows, kv, 0, M, n_heads, max_ctx, 0,
                                    (float *)ws, s);
   else
-    launch_decode_attention<float>((const float *)q, (float *)out, rows, kv, 0, M, n_heads, max_ctx, (float *)ws,
-                                   s);
+    launch_decode_attention<float>((const float *)q, (float *)out, rows, kv, 0, M, n_heads, max_ctx, 0,
+                                   (float *)ws, s);
   return op_status();
 }
 
