@@ -1,12 +1,16 @@
 // Weight GEMMs Y = X W^T (X: [M x K] activations, W: [N x K] weights, both
 // K-contiguous) with fused epilogues.
 //
-//  * gemm_skinny: bf16 MFMA for decode-sized M <= 64.  The weight matrix is the
-//    large operand and is streamed once from HBM with 16-byte loads straight
-//    into MFMA operand registers; four waves split the K range of a workgroup
-//    and are reduced through LDS; optional split-K across workgroups writes
-//    fp32 partials reduced by a finishing pass.
-//  * gemm_big: bf16 MFMA for prefill-sized M, 128x128x64 tiles staged in LDS.
+//  * gemm_skinny: 16-bit MFMA for decode-sized M <= 64.  The weight matrix is
+//    the large operand and is streamed once from HBM with 16-byte loads
+//    straight into MFMA operand registers, each wave owning 16 output columns
+//    over the workgroup's K range; optional split-K across workgroups writes
+//    fp32 partials that a finishing pass (or the next RMSNorm) reduces.
+//  * gemm_prefill: 16-bit MFMA for prefill-sized M when K is a multiple of
+//    128: 256x256 tiles, eight waves, two register stages of global loads
+//    ahead of double-buffered, XOR-swizzled LDS, optional split-K.
+//  * gemm_big: 16-bit MFMA for the remaining prefill shapes, 128x128x64 tiles
+//    staged in LDS.
 //  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
 #include <algorithm>
 
