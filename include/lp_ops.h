@@ -23,13 +23,29 @@ extern "C" {
 
 /* Y[M x N] (fp32, row stride N) = X[M x K] (row stride ldx) times W[N x K]^T:
  * the weight-GEMM contraction of every projection of the decoder (Q/K/V,
- * output, gate/up, down, LM head).  16-bit types with M <= 64 take the
- * decode kernel, larger M the prefill kernel; `k_splits` > 1 splits K across
- * workgroups (prefill: only when K is a multiple of 128; the count is rounded
- * to whole K chunks) and needs `ws` of at least k_splits * M * N * 4 bytes
- * (fp32 partials).  K must be a multiple of 8, N even; 16-byte aligned rows. */
+ * output, gate/up, down, LM head).  For LP_BF16 / LP_F16, W is in the tiled
+ * weight layout that lp_op_pack_weight writes; for LP_F32 it is row-major
+ * [N x K].  16-bit types with M <= 64 take the decode kernel, larger M the
+ * prefill kernel; `k_splits` > 1 splits K across workgroups (prefill: only
+ * when K is a multiple of 128; the count is rounded to whole K chunks) and
+ * needs `ws` of at least k_splits * M * N * 4 bytes (fp32 partials).  K must
+ * be a multiple of 8, N even; 16-byte aligned rows. */
 int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
                int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* The tiled weight layout of the 16-bit GEMMs (weights of Sec. II-A's
+ * decoder, stored for the decode phase's weight stream).  A row-major [N x K]
+ * matrix W (row n = output feature n, stride K, K % 8 == 0) becomes
+ * ceil(N/16) * ceil(K/32) tiles of 16 rows x 32 columns, 1024 elements each;
+ * tile (i, j) has index i * ceil(K/32) + j and holds rows 16i..16i+15,
+ * columns 32j..32j+31, its element (r, c) at position
+ * 8 * (r + 16 * (c / 8)) + c % 8.  Rows >= N and columns >= K are zero.
+ * lp_op_packed_weight_bytes gives the size (0 for other dtypes or
+ * non-positive sizes); lp_op_pack_weight writes W_packed (device, that many
+ * bytes, caller-owned, 16-byte aligned like W) on `hip_stream`.  LP_EINVAL for
+ * null pointers, bad sizes or a dtype other than LP_BF16 / LP_F16. */
+size_t lp_op_packed_weight_bytes(int32_t dtype, int32_t N, int32_t K);
+int lp_op_pack_weight(int32_t dtype, const void *W, void *W_packed, int32_t N, int32_t K, void *hip_stream);
 
 /* RMSNorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g for r < rows; x fp32
  * [rows x d] (first incremented in place by the n_part fp32 partial arrays

@@ -104,6 +104,12 @@ size_t part_bytes_for(const Dims &D, const lp_model_config &c, const lp_engine_o
   return m;
 }
 
+// Bytes of an [N x K] GEMM weight: the tiled layout for 16-bit models,
+// row-major fp32 otherwise.
+size_t wbytes(const Dims &D, int64_t N, int64_t K) {
+  return D.esz == 2 ? (size_t)wpack_elems(N, K) * 2 : (size_t)N * K * D.esz;
+}
+
 // Lays out everything but the KV pool size, which is decided by the caller.
 Layout plan_layout(const lp_model_config &c, const lp_engine_options &o, int64_t n_blocks) {
   const Dims D = dims_of(c);
@@ -117,14 +123,14 @@ Layout plan_layout(const lp_model_config &c, const lp_engine_options &o, int64_t
   Ly.embed = take((size_t)D.V * D.d * D.esz);
   for (int l = 0; l < D.L; ++l) {
     Ly.attn_norm.push_back(take((size_t)D.d * 4));
-    Ly.wqkv.push_back(take((size_t)D.qkv_n * D.d * D.esz));
-    Ly.wo.push_back(take((size_t)D.d * D.Hq * D.hd * D.esz));
+    Ly.wqkv.push_back(take(wbytes(D, D.qkv_n, D.d)));
+    Ly.wo.push_back(take(wbytes(D, D.d, (int64_t)D.Hq * D.hd)));
     Ly.mlp_norm.push_back(take((size_t)D.d * 4));
-    Ly.wgu.push_back(take((size_t)2 * D.F * D.d * D.esz));
-    Ly.wd.push_back(take((size_t)D.d * D.F * D.esz));
+    Ly.wgu.push_back(take(wbytes(D, 2 * (int64_t)D.F, D.d)));
+    Ly.wd.push_back(take(wbytes(D, D.d, D.F)));
   }
   Ly.final_norm = take((size_t)D.d * 4);
-  Ly.lm_head = take((size_t)D.V * D.d * D.esz);
+  Ly.lm_head = take(wbytes(D, D.V, D.d));
   Ly.weights_end = off;
   const int64_t R = rows_cap(o);
   const int max_pos = o.max_seq_len;
@@ -390,32 +396,49 @@ std::vector<TensorDesc> canonical(const Dims &D) {
   return t;
 }
 
-// Destination (byte offset of row 0, row permutation) of canonical tensor i.
+// Destination of canonical tensor i: byte offset of its row 0, row
+// permutation, whether it is a norm gain (fp32), and whether it is stored in
+// the tiled weight layout (every GEMM weight of a 16-bit model; the embedding
+// table stays row-major for the row gather).
 struct Dest {
   size_t off;
   int perm;
   bool gain;
+  bool packed;
 };
 
 Dest dest_of(const lp_engine *e, int i) {
   const Dims &D = e->D;
-  if (i == 0) return {e->Ly.embed, PERM_NONE, false};
+  const bool pk = D.esz == 2;
+  if (i == 0) return {e->Ly.embed, PERM_NONE, false, false};
   const int last = 1 + 9 * D.L;
-  if (i == last) return {e->Ly.final_norm, PERM_NONE, true};
-  if (i == last + 1) return {e->Ly.lm_head, PERM_NONE, false};
+  if (i == last) return {e->Ly.final_norm, PERM_NONE, true, false};
+  if (i == last + 1) return {e->Ly.lm_head, PERM_NONE, false, pk};
   const int l = (i - 1) / 9, j = (i - 1) % 9;
-  const size_t rowb = (size_t)D.d * D.esz;
+  // q, k and v start at whole 16-row slices, so their tiles are contiguous
+  // ranges of the fused matrix in either layout
+  const size_t rowb = (size_t)(pk ? wpack_kt(D.d) * WT_COLS : D.d) * D.esz;
   switch (j) {
-    case 0: return {e->Ly.attn_norm[l], PERM_NONE, true};
-    case 1: return {e->Ly.wqkv[l], PERM_ROPE, false};
-    case 2: return {e->Ly.wqkv[l] + (size_t)D.Hq * D.hd * rowb, PERM_ROPE, false};
-    case 3: return {e->Ly.wqkv[l] + (size_t)(D.Hq + D.Hkv) * D.hd * rowb, PERM_NONE, false};
-    case 4: return {e->Ly.wo[l], PERM_NONE, false};
-    case 5: return {e->Ly.mlp_norm[l], PERM_NONE, true};
-    case 6: return {e->Ly.wgu[l], PERM_GATE, false};
-    case 7: return {e->Ly.wgu[l], PERM_UP, false};
-    default: return {e->Ly.wd[l], PERM_NONE, false};
+    case 0: return {e->Ly.attn_norm[l], PERM_NONE, true, false};
+    case 1: return {e->Ly.wqkv[l], PERM_ROPE, false, pk};
+    case 2: return {e->Ly.wqkv[l] + (size_t)D.Hq * D.hd * rowb, PERM_ROPE, false, pk};
+    case 3: return {e->Ly.wqkv[l] + (size_t)(D.Hq + D.Hkv) * D.hd * rowb, PERM_NONE, false, pk};
+    case 4: return {e->Ly.wo[l], PERM_NONE, false, pk};
+    case 5: return {e->Ly.mlp_norm[l], PERM_NONE, true, false};
+    case 6: return {e->Ly.wgu[l], PERM_GATE, false, pk};
+    case 7: return {e->Ly.wgu[l], PERM_UP, false, pk};
+    default: return {e->Ly.wd[l], PERM_NONE, false, pk};
   }
+}
+
+// Host-side packing of a row-major rows x K matrix of 16-bit values into the
+// tiled weight layout (K % 8 == 0; padding zeroed).
+std::vector<uint16_t> pack_tiles(const uint16_t *src, int64_t rows, int64_t K) {
+  const int64_t kt = wpack_kt(K);
+  std::vector<uint16_t> out((size_t)wpack_elems(rows, K), 0);
+  for (int64_t n = 0; n < rows; ++n)
+    for (int64_t k = 0; k < K; k += 8) memcpy(&out[(size_t)wpack_off(n, k, kt)], src + n * K + k, 16);
+  return out;
 }
 
 int64_t perm_row(int perm, int64_t r, int hd) {
@@ -486,6 +509,23 @@ extern "C" int lp_load_weights(lp_engine *e, const void *blob, size_t bytes) {
         }
       }
       HIPCHK(e, hipMemcpy(e->arena + ds.off, g.data(), t.cols * 4, hipMemcpyHostToDevice));
+    } else if (ds.packed) {
+      // assemble the destination rows (q/k rotary pairs adjacent; gate and
+      // up, which follow each other in the blob, interleaved into rows 2f and
+      // 2f + 1), then tile them
+      if (ds.perm == PERM_UP) {  // written together with the gate rows
+        src += rowb * t.rows;
+        continue;
+      }
+      const int64_t out_rows = ds.perm == PERM_GATE ? 2 * t.rows : t.rows;
+      tmp.assign(rowb * out_rows, 0);
+      for (int64_t r = 0; r < t.rows; ++r) {
+        memcpy(tmp.data() + perm_row(ds.perm, r, D.hd) * rowb, src + r * rowb, rowb);
+        if (ds.perm == PERM_GATE)
+          memcpy(tmp.data() + perm_row(PERM_UP, r, D.hd) * rowb, src + (t.rows + r) * rowb, rowb);
+      }
+      const std::vector<uint16_t> pk = pack_tiles((const uint16_t *)tmp.data(), out_rows, t.cols);
+      HIPCHK(e, hipMemcpy(e->arena + ds.off, pk.data(), pk.size() * 2, hipMemcpyHostToDevice));
     } else if (ds.perm == PERM_NONE) {
       HIPCHK(e, hipMemcpy(e->arena + ds.off, src, rowb * t.rows, hipMemcpyHostToDevice));
     } else {
@@ -510,6 +550,10 @@ extern "C" int lp_init_weights_random(lp_engine *e, uint64_t seed, float stdv) {
   const Dims &D = e->D;
   auto ts = canonical(D);
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  // tiles past a matrix's last column (K not a multiple of 32) must read as
+  // zeros: the generator writes only the matrix's own elements
+  if (D.esz == 2 && (D.d % WT_COLS || D.F % WT_COLS || (D.Hq * D.hd) % WT_COLS))
+    HIPCHK(e, hipMemsetAsync(e->arena, 0, e->Ly.weights_end, e->stream));
   for (int i = 0; i < (int)ts.size(); ++i) {
     const auto &t = ts[i];
     const Dest ds = dest_of(e, i);
@@ -517,13 +561,13 @@ extern "C" int lp_init_weights_random(lp_engine *e, uint64_t seed, float stdv) {
       launch_fill_f32((float *)(e->arena + ds.off), t.cols, 1.0f, e->stream);
     } else if (D.act == ACT_F16) {
       launch_init_weight<f16_t>((f16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                ds.perm, D.hd, true, e->stream);
+                                ds.perm, D.hd, true, ds.packed, e->stream);
     } else if (D.act == ACT_BF16) {
       launch_init_weight<bf16_t>((bf16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                 ds.perm, D.hd, false, e->stream);
+                                 ds.perm, D.hd, false, ds.packed, e->stream);
     } else {
       launch_init_weight<float>((float *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                ds.perm, D.hd, false, e->stream);
+                                ds.perm, D.hd, false, false, e->stream);
     }
   }
   HIPCHK(e, hipGetLastError());

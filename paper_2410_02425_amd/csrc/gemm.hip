@@ -1,11 +1,15 @@
 // Weight GEMMs Y = X W^T (X: [M x K] activations, W: [N x K] weights, both
 // K-contiguous) with fused epilogues.
 //
+// 16-bit weights are in the tiled layout of kernels.hpp (16 x 32 tiles of
+// 1 KB in MFMA operand order); fp32 weights are row-major.
+//
 //  * gemm_skinny: 16-bit MFMA for decode-sized M <= 64.  The weight matrix is
-//    the large operand and is streamed once from HBM with 16-byte loads
-//    straight into MFMA operand registers, each wave owning 16 output columns
-//    over the workgroup's K range; optional split-K across workgroups writes
-//    fp32 partials that a finishing pass (or the next RMSNorm) reduces.
+//    the large operand and is streamed once from HBM, each wave reading its
+//    16-row slice tile after tile (1 KB contiguous per load) straight into
+//    MFMA operand registers over the workgroup's K range; optional split-K
+//    across workgroups writes fp32 partials that a finishing pass (or the
+//    next RMSNorm) reduces.
 //  * gemm_prefill: 16-bit MFMA for prefill-sized M when K is a multiple of
 //    128: 256x256 tiles, eight waves, two register stages of global loads
 //    ahead of double-buffered, XOR-swizzled LDS, optional split-K.
@@ -25,7 +29,11 @@ namespace lp {
 //
 // Decode-sized M (<= 64 rows, MT 16-row tiles).  The weight stream is the whole
 // cost: each wave owns NS 16-row slices of W and streams them over the
-// workgroup's K range, one sub-chunk (KSUB 32-wide k-steps) ahead of the MFMAs.
+// workgroup's K range, one sub-chunk (KSUB 32-wide k-steps, one weight tile
+// each) ahead of the MFMAs.  With the tiled layout every weight load is 1 KB
+// of contiguous memory and a slice is read front to back, which keeps the
+// HBM pages that the concurrent waves stream open far longer than 64-byte
+// pieces of 16 separate rows would.
 // The activations of a sub-chunk are staged once per workgroup into LDS in
 // MFMA-fragment order (one 1 KB block per (k-step, m-tile), lane-major), so
 // they never occupy the vector-memory counter the weight prefetch waits on.
@@ -51,7 +59,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
   __shared__ u32x4_t xs0[KSUB][MT][64];
   __shared__ u32x4_t xs1[KSUB][MT][64];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  const int r16 = lane & 15;
   const int n0 = (blockIdx.x * NW + wave) * NS * 16;
   const int kbeg = blockIdx.y * kchunk, kend = min(K, kbeg + kchunk);
   const int nsub = ((kend - kbeg + 2 * KC - 1) / (2 * KC)) * 2;
@@ -59,9 +67,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
 #define SK_SC(c) (kbeg + (((c) + rot) % nsub) * KC)
   const int klast = SK_SC(nsub - 1);
 
+  const int64_t wkt = wpack_kt(K);
+  const int nsl = (N + WT_ROWS - 1) / WT_ROWS;  // 16-row slices of W
   const T *wrow[NS];
 #pragma unroll
-  for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min(n0 + j * 16 + r16, N - 1) * K;
+  for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min((n0 >> 4) + j, nsl - 1) * wkt * WT_ELEMS + lane * 8;
   const T *xsrc[XF];
   int xk[XF];
 #pragma unroll
@@ -90,8 +100,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
   }
 #define SK_WLOAD(WB, kb)                                                                        \
   _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
-    const int kk = min((kb) + ks * 32 + kq, K - 8);                                             \
-    _Pragma("unroll") for (int j = 0; j < NS; ++j) WB[ks][j] = load8<T>(wrow[j] + kk);          \
+    const int64_t t = min((int64_t)((kb) >> 5) + ks, wkt - 1);                                  \
+    _Pragma("unroll") for (int j = 0; j < NS; ++j) WB[ks][j] = load8<T>(wrow[j] + t * WT_ELEMS); \
   }
 #define SK_MMA(WB, XS)                                                                          \
   _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
@@ -192,6 +202,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * BG_BM, n0 = blockIdx.x * BG_BN;
+  const int64_t wkt = wpack_kt(K);
 
   // global -> register staging: each thread moves 4 chunks of 16 B for A and B
   uint4 ra[4], rb[4];
@@ -201,7 +212,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
     const int row = idx >> 3, kk = (k0) + (idx & 7) * 8;                                        \
     const int m = m0 + row, n = n0 + row;                                                       \
     ra[c] = (m < M && kk < K) ? *(const uint4 *)(X + (int64_t)m * ldx + kk) : make_uint4(0, 0, 0, 0); \
-    rb[c] = (n < N && kk < K) ? *(const uint4 *)(W + (int64_t)n * K + kk) : make_uint4(0, 0, 0, 0);   \
+    rb[c] = (n < N && kk < K) ? *(const uint4 *)(W + wpack_off(n, kk, wkt)) : make_uint4(0, 0, 0, 0); \
   }
   floatx16_t acc[2][2];
 #pragma unroll
@@ -270,7 +281,8 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // the staged tile goes to one of two LDS buffers.  LDS rows are 128 bytes
 // (one K stage) with the sixteen-byte chunks XOR-swizzled by row, so that the
 // coalesced row stores and the 32-row MFMA fragment reads are both free of
-// bank conflicts.  gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the
+// bank conflicts; a weight stage is two consecutive tiles of each 16-row
+// slice.  gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the
 // epilogue.  Rows and columns past M / N read clamped (valid) memory and are
 // never stored; K must be a multiple of 128 (an even number of stages per
 // split).
@@ -303,10 +315,12 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
     ga[i] = X + (int64_t)min(m0 + row, M - 1) * ldx + kb + c * 8;
     la[i] = pf_swz(row, c);
   }
+  // W tiles: a 64-wide K stage is two consecutive 1 KB tiles of each slice
+  const int64_t wkt = wpack_kt(K);
 #pragma unroll
   for (int i = 0; i < CB; ++i) {
     const int idx = tid + i * PF_NT, row = idx >> 3, c = idx & 7;
-    gb[i] = W + (int64_t)min(n0 + row, N - 1) * K + kb + c * 8;
+    gb[i] = W + wpack_off(min(n0 + row, N - 1), kb + c * 8, wkt);
     lb[i] = PF_BM * PF_BK + pf_swz(row, c);
   }
   u32x4_t r0a[CA], r0b[CB], r1a[CA], r1b[CB];
@@ -326,7 +340,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 
 #define PF_LOAD(RA, RB, kt)                                                                        \
   _Pragma("unroll") for (int i = 0; i < CA; ++i) RA[i] = *(const u32x4_t *)(ga[i] + (kt) * PF_BK); \
-  _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = *(const u32x4_t *)(gb[i] + (kt) * PF_BK);
+  _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = *(const u32x4_t *)(gb[i] + (kt) * (PF_BK / WT_COLS) * WT_ELEMS);
 #define PF_STORE(RA, RB, buf)                                                                      \
   _Pragma("unroll") for (int i = 0; i < CA; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + la[i]) = RA[i]; \
   _Pragma("unroll") for (int i = 0; i < CB; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + lb[i]) = RB[i];
@@ -570,6 +584,31 @@ void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int 
   dim3 grid((N + F_BN - 1) / F_BN, (M + F_BM - 1) / F_BM);
   launch_k(gemm_f32_kernel, grid, 256, s, timing, X, ldx, W, M, N, K, ep);
 }
+
+// ------------------------------------------------------------------ weight packing
+
+// One thread per 16-byte piece of the tiled output: piece p is lane p % 64 of
+// tile p / 64.  Pieces past N or K are written as zeros.  K % 8 == 0.
+template <typename T>
+__global__ void wpack_kernel(const T *__restrict__ src, T *__restrict__ dst, int N, int K, int64_t pieces) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= pieces) return;
+  const int64_t kt = wpack_kt(K), t = p >> 6;
+  const int l = (int)(p & 63);
+  const int64_t n = (t / kt) * WT_ROWS + (l & 15), k = (t % kt) * WT_COLS + (l >> 4) * 8;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (n < N && k < K) v = *(const uint4 *)(src + n * K + k);
+  *(uint4 *)(dst + p * 8) = v;
+}
+
+template <typename T>
+void launch_wpack(const T *src, T *dst, int N, int K, hipStream_t s) {
+  const int64_t pieces = wpack_elems(N, K) / 8;
+  if (pieces > 0) wpack_kernel<T><<<(unsigned)((pieces + 255) / 256), 256, 0, s>>>(src, dst, N, K, pieces);
+}
+
+template void launch_wpack<bf16_t>(const bf16_t *, bf16_t *, int, int, hipStream_t);
+template void launch_wpack<f16_t>(const f16_t *, f16_t *, int, int, hipStream_t);
 
 template void launch_gemm_finish<float>(const float *, int, int, int, const Epi &, hipStream_t);
 template void launch_gemm_finish<bf16_t>(const float *, int, int, int, const Epi &, hipStream_t);

@@ -12,6 +12,25 @@ constexpr int KV_BLOCK = 64;  // tokens per KV-cache block
 typedef uint16_t bf16_t;
 typedef _Float16 f16_t;
 
+// Tiled layout of 16-bit weight matrices, read by every 16-bit GEMM kernel.
+// An [N x K] matrix (row n is output feature n, K its inputs) is cut into
+// tiles of 16 rows x 32 columns, 1 KB each.  Tile (i, j) holds rows
+// 16i..16i+15 and columns 32j..32j+31 and has index i * ceil(K/32) + j, so
+// the tiles of one 16-row slice follow each other along K.  Inside a tile the
+// 8 elements of lane l = r + 16q (r < 16, q < 4) are row 16i + r, columns
+// 32j + 8q .. 32j + 8q + 7: the B operand of a 16x16x32 MFMA, so a wave reads
+// a tile with one contiguous 1 KB load and streams a slice front to back.
+// Rows past N and columns past K are zero.
+constexpr int WT_ROWS = 16, WT_COLS = 32, WT_ELEMS = WT_ROWS * WT_COLS;
+__host__ __device__ inline int64_t wpack_kt(int64_t K) { return (K + WT_COLS - 1) / WT_COLS; }
+__host__ __device__ inline int64_t wpack_elems(int64_t N, int64_t K) {
+  return (N + WT_ROWS - 1) / WT_ROWS * wpack_kt(K) * WT_ELEMS;
+}
+// Element offset of (n, k) for a matrix with kt = wpack_kt(K) tiles along K.
+__host__ __device__ inline int64_t wpack_off(int64_t n, int64_t k, int64_t kt) {
+  return ((n >> 4) * kt + (k >> 5)) * WT_ELEMS + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+}
+
 // Where the rows of a step read their token and write their results.
 struct RowMeta {
   const int32_t *row_slot;  // [M] KV slot of each row
@@ -69,7 +88,8 @@ void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride
                     const int32_t *rows, const float *g, T *y, int M, int d, float eps,
                     hipStream_t s);
 
-// Generic GEMM Y = X W^T with epilogue.  T = float, bf16_t or f16_t.
+// Generic GEMM Y = X W^T with epilogue.  T = float, bf16_t or f16_t.  W is
+// in the tiled weight layout for 16-bit T, row-major [N x K] for float.
 // splits > 1 (16-bit only): writes partials [splits][M][N] into `part` and a
 // following launch_gemm_finish (or an RMSNorm fold) applies the epilogue;
 // gemm_effective_splits gives the count a launch uses for a requested one.
@@ -83,6 +103,11 @@ int gemm_effective_splits(int M, int N, int K, int splits);
 // K splits the prefill GEMM (M > 64) takes for its shape (1 when the tile grid
 // fills the chip); an effective count.
 int prefill_gemm_splits(int M, int N, int K);
+
+// Packs a row-major [N x K] 16-bit matrix (row stride K) into the tiled
+// weight layout at dst (wpack_elems(N, K) elements, padding zeroed).
+template <typename T>
+void launch_wpack(const T *src, T *dst, int N, int K, hipStream_t s);
 
 template <typename T>
 void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s);
@@ -127,12 +152,14 @@ void launch_sample(const float *logits, int64_t ld, int M, int V, const SamplePa
                    int32_t *slot_tok, int32_t *tok_out, hipStream_t s);
 
 // Weight generator: writes rows x cols values of canonical tensor `tensor_id`
-// to dst with row r stored at perm(r), in T.  `bf16_values`: round each value
+// to dst with row r stored at perm(r), in T, row-major or (`packed`) in the
+// tiled weight layout of a cols-wide matrix.  `bf16_values`: round each value
 // to bf16 first (a bf16 model held in fp16 storage keeps its exact values).
 enum RowPerm : int { PERM_NONE = 0, PERM_ROPE = 1, PERM_GATE = 2, PERM_UP = 3 };
 template <typename T>
 void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
-                        int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, hipStream_t s);
+                        int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, bool packed,
+                        hipStream_t s);
 void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s);
 
 }  // namespace lp

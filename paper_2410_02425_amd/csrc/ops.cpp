@@ -57,6 +57,22 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
   return op_status();
 }
 
+extern "C" size_t lp_op_packed_weight_bytes(int32_t dtype, int32_t N, int32_t K) {
+  if ((dtype != LP_BF16 && dtype != LP_F16) || N <= 0 || K <= 0) return 0;
+  return (size_t)wpack_elems(N, K) * 2;
+}
+
+extern "C" int lp_op_pack_weight(int32_t dtype, const void *W, void *W_packed, int32_t N, int32_t K, void *stream) {
+  OPCHK(W && W_packed && N > 0 && K > 0 && K % 8 == 0, "pack weight: bad pointers or sizes (K % 8 == 0)");
+  OPCHK(dtype == LP_BF16 || dtype == LP_F16, "pack weight: 16-bit dtypes only");
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LP_BF16)
+    launch_wpack<bf16_t>((const bf16_t *)W, (bf16_t *)W_packed, N, K, s);
+  else
+    launch_wpack<f16_t>((const f16_t *)W, (f16_t *)W_packed, N, K, s);
+  return op_status();
+}
+
 extern "C" int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t n_part, const float *g, void *y,
                              int32_t rows, int32_t d, float eps, void *stream) {
   OPCHK(x && g && y && rows >= 0 && d > 0 && d <= 8192 && n_part >= 0 && (n_part == 0 || part), "rmsnorm: args");
@@ -155,13 +171,13 @@ extern "C" int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
     launch_init_weight<bf16_t>((bf16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
-                               cols, stdv, PERM_NONE, 0, false, s);
+                               cols, stdv, PERM_NONE, 0, false, false, s);
   else if (dtype == LP_F16)
     launch_init_weight<f16_t>((f16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
-                              cols, stdv, PERM_NONE, 0, true, s);
+                              cols, stdv, PERM_NONE, 0, true, false, s);
   else if (dtype == LP_F32)
     launch_init_weight<float>((float *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows, cols,
-                              stdv, PERM_NONE, 0, false, s);
+                              stdv, PERM_NONE, 0, false, false, s);
   else
     OPCHK(false, "init_weight: dtype");
   return op_status();

@@ -24,7 +24,7 @@ EXPORTED = [
     "lp_get_token_times", "lp_get_run_stats", "lp_get_step_log", "lp_get_logits", "lp_last_error",
     "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
     "lp_wg_fit", "lp_wg_info", "lp_wg_bins", "lp_wg_sample", "lp_wg_sample_independent", "lp_wg_free",
-    "lp_op_gemm", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
+    "lp_op_gemm", "lp_op_packed_weight_bytes", "lp_op_pack_weight", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
     "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight", "lp_op_sample",
 ]
 
@@ -115,6 +115,7 @@ def lib():
             "lp_wg_sample_independent": [vp, P(C.c_double), i64, P(C.c_double)],
             "lp_get_latency_summary": [vp, P(LatencySummary)],
             "lp_op_gemm": [i32, vp, i64, vp, vp, i32, i32, i32, i32, vp, sz, vp],
+            "lp_op_pack_weight": [i32, vp, vp, i32, i32, vp],
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
             "lp_op_decode_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp, sz,
                                        vp],
@@ -131,6 +132,8 @@ def lib():
         L.lp_last_error.restype = C.c_char_p
         L.lp_op_decode_attention_ws_bytes.argtypes = [i32, i32, i32, i32]
         L.lp_op_decode_attention_ws_bytes.restype = sz
+        L.lp_op_packed_weight_bytes.argtypes = [i32, i32, i32]
+        L.lp_op_packed_weight_bytes.restype = sz
         L.lp_engine_destroy.restype = None
         L.lp_wg_free.argtypes = [vp]
         L.lp_wg_free.restype = None
@@ -408,9 +411,25 @@ def _dt(t):
     return LP_BF16 if t.dtype in (torch.bfloat16, torch.int16, torch.uint16) else LP_F32
 
 
-def op_gemm(X, W, Y, k_splits=1, ws=None):
+def packed_weight_elems(N: int, K: int) -> int:
+    """Elements of an [N x K] 16-bit weight in the tiled layout."""
+    return -(-N // 16) * -(-K // 32) * 512
+
+
+def op_pack_weight(W, W_packed):
+    """Row-major [N x K] 16-bit W -> the tiled layout the 16-bit GEMMs read
+    (W_packed: a flat tensor of packed_weight_elems(N, K) elements)."""
+    N, K = W.shape
+    assert W_packed.numel() * W_packed.element_size() >= lib().lp_op_packed_weight_bytes(_dt(W), N, K)
+    _check(lib().lp_op_pack_weight(_dt(W), _ptr(W), _ptr(W_packed), N, K, _stream()))
+
+
+def op_gemm(X, W, Y, k_splits=1, ws=None, N=None):
+    """Y = X W^T.  16-bit: W is the packed flat tensor and N its row count;
+    fp32: W is row-major [N x K]."""
     M, K = X.shape
-    N = W.shape[0]
+    if N is None:
+        N = W.shape[0]
     _check(lib().lp_op_gemm(_dt(X), _ptr(X), X.stride(0), _ptr(W), _ptr(Y), M, N, K, k_splits, _ptr(ws),
                             0 if ws is None else ws.numel() * ws.element_size(), _stream()))
 

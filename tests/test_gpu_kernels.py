@@ -44,6 +44,46 @@ GEMM_CASES = [
 HALF = {"bf16": torch.bfloat16, "f16": torch.float16}
 
 
+def packed(Wd):
+    """W (device, row-major [N x K], 16-bit) in the tiled weight layout."""
+    N, K = Wd.shape
+    P = torch.full((lp.packed_weight_elems(N, K),), float("nan"), dtype=Wd.dtype, device=DEV)
+    lp.op_pack_weight(Wd, P)
+    return P
+
+
+def tile_layout_reference(W):
+    """The tiled layout written out from its definition: tiles of 16 rows x 32
+    columns, tile (i, j) at index i * ceil(K/32) + j, element (r, c) of a tile
+    at 8 * (r + 16 * (c // 8)) + c % 8, zeros past N and K."""
+    N, K = W.shape
+    nt, kt = -(-N // 16), -(-K // 32)
+    full = np.zeros((nt * 16, kt * 32), dtype=W.dtype)
+    full[:N, :K] = W
+    out = np.zeros(nt * kt * 512, dtype=W.dtype)
+    for i in range(nt):
+        for j in range(kt):
+            tile = full[16 * i:16 * i + 16, 32 * j:32 * j + 32]
+            base = (i * kt + j) * 512
+            for r in range(16):
+                for c in range(32):
+                    out[base + 8 * (r + 16 * (c // 8)) + c % 8] = tile[r, c]
+    return out
+
+
+@pytest.mark.parametrize("half", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (50, 40), (1000, 1000), (33, 688)])
+def test_pack_weight_layout(N, K, half):
+    rng = np.random.default_rng(N * 31 + K)
+    Wd = to_dev(bf16_values(rng, (N, K)), HALF[half])
+    P = packed(Wd)
+    torch.cuda.synchronize()
+    got = P.float().cpu().numpy()
+    want = tile_layout_reference(Wd.float().cpu().numpy())  # the values as stored in the half type
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)                 # bit-exact, padding zero (no NaN left)
+
+
 @pytest.mark.parametrize("half", ["bf16", "f16"])
 @pytest.mark.parametrize("M,N,K,splits", GEMM_CASES)
 def test_gemm_16bit(M, N, K, splits, half):
@@ -53,7 +93,7 @@ def test_gemm_16bit(M, N, K, splits, half):
     Xd, Wd = to_dev(X, HALF[half]), to_dev(W, HALF[half])
     Y = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
     ws = torch.empty(max(splits, 1) * M * N, dtype=torch.float32, device=DEV)
-    lp.op_gemm(Xd, Wd, Y, splits, ws)
+    lp.op_gemm(Xd, packed(Wd), Y, splits, ws, N=N)
     torch.cuda.synchronize()
     got = Y.cpu().numpy()
     ref = X.astype(np.float64) @ W.astype(np.float64).T
@@ -70,7 +110,7 @@ def test_gemm_full_8b_gate_up_sampled(half):
     X = torch.randn(M, K, generator=g).to(HALF[half])
     W = (torch.randn(N, K, generator=g) * 0.02).to(HALF[half])
     Y = torch.empty(M, N, dtype=torch.float32, device=DEV)
-    lp.op_gemm(X.to(DEV), W.to(DEV), Y, 1, None)
+    lp.op_gemm(X.to(DEV), packed(W.to(DEV)), Y, 1, None, N=N)
     torch.cuda.synchronize()
     rng = np.random.default_rng(0)
     rows, cols = rng.integers(0, M, 512), rng.integers(0, N, 512)
