@@ -480,9 +480,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 
 // ------------------------------------------------------------------ dispatch
 
-// Launch shapes of the decode kernel, chosen from the weight matrix shape:
-// one 16-column slice per wave, eight waves per workgroup sharing the staged
-// activations, and (for the largest N) sixteen waves with deeper sub-chunks.
+// Launch shapes of the decode kernel, chosen from the weight matrix shape by
+// measured sweeps: one 16-column slice per wave and two weight tiles per
+// sub-chunk, eight waves per workgroup sharing the staged activations; for
+// the largest N (the LM head) sixteen waves with one tile per sub-chunk.
 struct SkinnyPlan {
   int ns, ksub, nw, splits, kchunk;
 };
@@ -490,7 +491,7 @@ struct SkinnyPlan {
 SkinnyPlan skinny_plan(int N, int K, int want_splits) {
   SkinnyPlan p;
   if (N >= 65536) {
-    p = {1, 4, 16, 1, 0};
+    p = {1, 1, 16, 1, 0};
   } else {
     p = {1, 2, 8, 1, 0};
   }
@@ -530,7 +531,7 @@ static void launch_skinny_mt(const T *X, int64_t ldx, const T *W, int M, int N, 
   const int cols = p.nw * p.ns * 16;
   dim3 grid((N + cols - 1) / cols, p.splits);
   if (p.nw == 16)
-    launch_k(gemm_skinny_kernel<T, MT, 1, 4, 16, false>, grid, 16 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
+    launch_k(gemm_skinny_kernel<T, MT, 1, 1, 16, false>, grid, 16 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
              part, ep);
   else if (ep.kind == EPI_SILU && p.splits == 1)
     launch_k(gemm_skinny_kernel<T, MT, 1, 2, 8, true>, grid, 8 * 64, s, timing, X, ldx, W, M, N, K, p.kchunk,
