@@ -46,16 +46,23 @@ GATE_UP_TRAFFIC = {"bytes_per_launch": 238320347, "kernel_source": "327a08e079c0
 
 
 def skinny_kernel_fingerprint() -> str:
-    """sha256 prefix of the decode GEMM kernel's source text: its section of
-    gemm.hip, its launch plan, and the device helpers it includes."""
+    """sha256 prefix of the source text the decode GEMM launch executes: the
+    kernel's section of gemm.hip, its launch plan and launcher, the tiled
+    weight layout helpers of kernels.hpp, and the device helpers."""
     csrc = os.path.join(ROOT, "paper_2410_02425_amd", "csrc")
     s = open(os.path.join(csrc, "gemm.hip")).read()
-    a = s.index("// ------------------------------------------------------------------ skinny (decode)")
-    b = s.index("// ------------------------------------------------------------------ split-K finish")
-    c = s.index("struct SkinnyPlan {")
-    e = s.index("static void launch_gemm_mfma(")
-    d = open(os.path.join(csrc, "device.hpp")).read()
-    return hashlib.sha256((s[a:b] + s[c:e] + d).encode()).hexdigest()[:16]
+    h = open(os.path.join(csrc, "kernels.hpp")).read()
+
+    def cut(text, start, end):
+        a = text.index(start)
+        return text[a:text.index(end, a)]
+    parts = [cut(s, "// ------------------------------------------------------------------ skinny (decode)",
+                 "// ------------------------------------------------------------------ split-K finish"),
+             cut(s, "struct SkinnyPlan {", "int skinny_effective_splits("),
+             cut(s, "template <typename T, int MT>\nstatic void launch_skinny_mt(", "template <typename T>\nstatic"),
+             cut(h, "// Tiled layout of 16-bit weight matrices", "// Where the rows of a step read"),
+             open(os.path.join(csrc, "device.hpp")).read()]
+    return hashlib.sha256("".join(parts).encode()).hexdigest()[:16]
 
 
 def decode_step_bytes(shape: synth.ModelShape, rows: int, sum_ctx: int, esz: int = 2) -> int:

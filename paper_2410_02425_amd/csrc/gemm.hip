@@ -11,8 +11,9 @@
 //    across workgroups writes fp32 partials that a finishing pass (or the
 //    next RMSNorm) reduces.
 //  * gemm_prefill: 16-bit MFMA for prefill-sized M when K is a multiple of
-//    128: 256x256 tiles, eight waves, two register stages of global loads
-//    ahead of double-buffered, XOR-swizzled LDS, optional split-K.
+//    128: 256x256 tiles, eight waves, operands loaded straight from global
+//    memory into four LDS stage buffers (three stages in flight), weight
+//    tiles used verbatim as MFMA operands, optional split-K.
 //  * gemm_big: 16-bit MFMA for the remaining prefill shapes, 128x128x64 tiles
 //    staged in LDS.
 //  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
@@ -275,140 +276,142 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 
 // ------------------------------------------------------------------ prefill (M > 64)
 //
-// 256x256 output tiles, eight waves (4 x 2, each 64 x 128 = 2 x 4 MFMA 32x32x16
-// tiles), 64-wide K stages.  Global loads run two stages ahead of the MFMAs
-// in two register sets, so each load has two stages of MFMA work to land in;
-// the staged tile goes to one of two LDS buffers.  LDS rows are 128 bytes
-// (one K stage) with the sixteen-byte chunks XOR-swizzled by row, so that the
-// coalesced row stores and the 32-row MFMA fragment reads are both free of
-// bank conflicts; a weight stage is two consecutive tiles of each 16-row
-// slice.  gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the
-// epilogue.  Rows and columns past M / N read clamped (valid) memory and are
-// never stored; K must be a multiple of 128 (an even number of stages per
-// split).
+// 256x256 output tiles, eight waves (4 x 2, each 64 x 128 = 4 x 8 MFMA
+// 16x16x32 tiles), 32-wide K stages.  Operands travel from global memory
+// straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
+// the instruction's LDS base + 16 x lane), with no register staging and no LDS
+// store instructions.  Four stage buffers, three stages in flight: at each
+// stage a wave waits for its own loads of that stage (the in-order vmcnt
+// counter, with the two younger stages still outstanding), then a barrier
+// makes every wave's loads visible, and the buffer freed by the previous
+// stage is refilled before the MFMAs run.
+//   * A weight stage is one tile per 16-row slice, copied verbatim: its lanes
+//     are already the B operand of a 16x16x32 MFMA.
+//   * An activation stage holds 256 rows of 64 bytes.  The four 16-byte
+//     chunks of row r are stored XOR-swizzled by (r / 4) % 4, by choosing the
+//     global address each lane loads, so that the 16-row fragment reads are
+//     free of bank conflicts.
+// gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the epilogue.  Rows
+// and columns past M / N read clamped (valid) memory and are never stored;
+// loads past the last stage re-read it into a buffer nobody reads, so every
+// wave's load count (and the wait count) is the same at every stage.  K must
+// be a multiple of 128.
 
-constexpr int PF_BM = 256, PF_BN = 256, PF_BK = 64, PF_WM = 4, PF_WN = 2, PF_NT = PF_WM * PF_WN * 64;
-constexpr int PF_STAGE = (PF_BM + PF_BN) * PF_BK;  // elements per LDS buffer
+constexpr int PF_BM = 256, PF_BN = 256, PF_BK = 32, PF_NB = 4, PF_NT = 512;
+constexpr int PF_KQ = 128;                          // K granularity of a split
+constexpr int PF_ABYTES = PF_BM * PF_BK * 2;        // activation bytes per stage
+constexpr int PF_SBYTES = (PF_BM + PF_BN) * PF_BK * 2;  // bytes per stage buffer
 
-__device__ __forceinline__ int pf_swz(int row, int c) { return row * PF_BK + ((c ^ (row & 7)) << 3); }
+// 16 bytes per lane from global memory into LDS at `lds` (wave-uniform byte
+// address) + 16 x lane.  The load is invisible to the compiler's wait-count
+// tracking; the prefill kernel waits for it explicitly.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory", "m0");
+}
 
 template <typename T>
 __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
                                                              int kchunk, float *__restrict__ part, Epi ep) {
   typedef typename Mfma<T>::v8 v8;
-  constexpr int TM = PF_BM / PF_WM / 32, TN = PF_BN / PF_WN / 32;  // MFMA tiles per wave
-  constexpr int CA = PF_BM * 8 / PF_NT, CB = PF_BN * 8 / PF_NT;   // 16-byte chunks per thread
-  __shared__ __attribute__((aligned(16))) T lds[2 * PF_STAGE];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = wave / PF_WN, wn = wave % PF_WN;
+  __shared__ __attribute__((aligned(1024))) char lds[PF_NB * PF_SBYTES];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * PF_BM, n0 = blockIdx.x * PF_BN;
   const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
   const int nk = (ke - kb) / PF_BK;
-
-  const T *ga[CA];
-  const T *gb[CB];
-  int la[CA], lb[CB];
-#pragma unroll
-  for (int i = 0; i < CA; ++i) {
-    const int idx = tid + i * PF_NT, row = idx >> 3, c = idx & 7;
-    ga[i] = X + (int64_t)min(m0 + row, M - 1) * ldx + kb + c * 8;
-    la[i] = pf_swz(row, c);
-  }
-  // W tiles: a 64-wide K stage is two consecutive 1 KB tiles of each slice
   const int64_t wkt = wpack_kt(K);
-#pragma unroll
-  for (int i = 0; i < CB; ++i) {
-    const int idx = tid + i * PF_NT, row = idx >> 3, c = idx & 7;
-    gb[i] = W + wpack_off(min(n0 + row, N - 1), kb + c * 8, wkt);
-    lb[i] = PF_BM * PF_BK + pf_swz(row, c);
-  }
-  u32x4_t r0a[CA], r0b[CB], r1a[CA], r1b[CB];
-  floatx16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  int fa[TM], fb[TN];  // LDS rows of this lane's fragments
-#pragma unroll
-  for (int i = 0; i < TM; ++i) fa[i] = wm * (PF_BM / PF_WM) + i * 32 + (lane & 31);
-#pragma unroll
-  for (int j = 0; j < TN; ++j) fb[j] = wn * (PF_BN / PF_WN) + j * 32 + (lane & 31);
-  const int kh = lane >> 5;
+  const int nsl = (N + WT_ROWS - 1) / WT_ROWS;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)lds;
 
-#define PF_LOAD(RA, RB, kt)                                                                        \
-  _Pragma("unroll") for (int i = 0; i < CA; ++i) RA[i] = *(const u32x4_t *)(ga[i] + (kt) * PF_BK); \
-  _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = *(const u32x4_t *)(gb[i] + (kt) * (PF_BK / WT_COLS) * WT_ELEMS);
-#define PF_STORE(RA, RB, buf)                                                                      \
-  _Pragma("unroll") for (int i = 0; i < CA; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + la[i]) = RA[i]; \
-  _Pragma("unroll") for (int i = 0; i < CB; ++i) *(u32x4_t *)(lds + (buf) * PF_STAGE + lb[i]) = RB[i];
-#define PF_MMA(buf)                                                                                \
-  _Pragma("unroll") for (int ks = 0; ks < PF_BK / 16; ++ks) {                                      \
-    v8 a[TM], b[TN];                                                                               \
-    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                 \
-      a[i] = load8<T>(lds + (buf) * PF_STAGE + pf_swz(fa[i], ks * 2 + kh));                        \
-    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                 \
-      b[j] = load8<T>(lds + (buf) * PF_STAGE + PF_BM * PF_BK + pf_swz(fb[j], ks * 2 + kh));        \
-    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                 \
-    _Pragma("unroll") for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::m32(a[i], b[j], acc[i][j]); \
+  // this wave's share of a stage: two 1 KB blocks of activations (16 rows
+  // each) and two weight tiles
+  const T *ga[2];
+  const T *gw[2];
+  uint32_t la[2], lw[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int blk = wave * 2 + i;
+    const int row = blk * 16 + (lane >> 2), slot = lane & 3;
+    const int q = slot ^ ((row >> 2) & 3);  // the K chunk that this LDS slot holds
+    ga[i] = X + (int64_t)min(m0 + row, M - 1) * ldx + kb + q * 8;
+    la[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + blk * 1024));
+    gw[i] = W + ((int64_t)min((n0 >> 4) + blk, nsl - 1) * wkt + kb / WT_COLS) * WT_ELEMS + lane * 8;
+    lw[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + PF_ABYTES + blk * 1024));
   }
-
-  // stage s is loaded into register set s % 2 two stages before its MFMAs
-  PF_LOAD(r0a, r0b, 0)
-  PF_LOAD(r1a, r1b, min(1, nk - 1))
-  PF_STORE(r0a, r0b, 0)
-  PF_LOAD(r0a, r0b, min(2, nk - 1))
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    PF_MMA(0)
-    PF_STORE(r1a, r1b, 1)
-    PF_LOAD(r1a, r1b, min(kt + 3, nk - 1))
-    __syncthreads();
-    PF_MMA(1)
-    PF_STORE(r0a, r0b, 0)
-    PF_LOAD(r0a, r0b, min(kt + 4, nk - 1))
-    __syncthreads();
+#define PF_ISSUE(kt)                                                                                 \
+  {                                                                                                  \
+    const int s_ = min((kt), nk - 1);                                                                \
+    const uint32_t b_ = (uint32_t)(((kt) & (PF_NB - 1)) * PF_SBYTES);                                \
+    _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(ga[i] + s_ * PF_BK, la[i] + b_);             \
+    _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(gw[i] + (int64_t)s_ * WT_ELEMS, lw[i] + b_); \
   }
-#undef PF_LOAD
-#undef PF_STORE
-#undef PF_MMA
+  floatx4_t acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  int fa[4];  // byte offsets of this lane's activation fragments in a stage
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = wm * 64 + i * 16 + (lane & 15), q = lane >> 4;
+    fa[i] = r * 64 + ((q ^ ((r >> 2) & 3)) << 4);
+  }
+  const int fb = PF_ABYTES + wn * 8 * 1024 + lane * 16;
 
-  // accumulator (i, j, r) of lane l: row (r & 3) + 4 (l / 32) + 8 (r / 4), column l % 32
-  const int wrow = m0 + wm * (PF_BM / PF_WM), wcol = n0 + wn * (PF_BN / PF_WN);
+  PF_ISSUE(0)
+  PF_ISSUE(1)
+  PF_ISSUE(2)
+  for (int kt = 0; kt < nk; ++kt) {
+    // 4 loads per stage and wave: at most 8 outstanding = stage kt has landed
+    asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    PF_ISSUE(kt + 3)
+    const char *st = lds + (kt & (PF_NB - 1)) * PF_SBYTES;
+    v8 a[4], b[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = *(const v8 *)(st + fa[i]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = *(const v8 *)(st + fb + j * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = Mfma<T>::m16(a[i], b[j], acc[i][j]);
+  }
+#undef PF_ISSUE
+  // the last (re-read) stages land before LDS is reused below
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  // accumulator (i, j) of lane l: row 4 (l / 16) + r of 16-row tile i, column l % 16 of tile j
+  const int wrow = m0 + wm * 64, wcol = n0 + wn * 128;
   if (gridDim.z > 1) {
     float *pz = part + (int64_t)blockIdx.z * M * N;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = wcol + j * 32 + (lane & 31);
+      for (int j = 0; j < 8; ++j) {
+        const int n = wcol + j * 16 + (lane & 15);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = wrow + i * 32 + (r & 3) + 4 * (lane >> 5) + 8 * (r >> 2);
+        for (int r = 0; r < 4; ++r) {
+          const int m = wrow + i * 16 + (lane >> 4) * 4 + r;
           if (m < M && n < N) pz[(int64_t)m * N + n] = acc[i][j][r];
         }
       }
     return;
   }
-  // epilogue through LDS (free after the last stage): each wave stages 32 rows
-  // x 128 columns of fp32 at a time in its own 16 KB, then its lanes apply the
-  // epilogue to column pairs, one 128-column row per pass of the wave
-  constexpr int SROW = PF_BN / PF_WN;  // fp32 row stride of the staging tile
-  static_assert(PF_WM * PF_WN * 32 * SROW * 4 <= 2 * PF_STAGE * (int)sizeof(T), "staging fits in LDS");
-  float *stg = (float *)lds + wave * 32 * SROW;
+  // epilogue through LDS: each wave stages 16 rows x 128 columns of fp32 at a
+  // time in its own 8 KB, then its lanes apply the epilogue to column pairs,
+  // one 128-column row per pass of the wave
+  float *stg = (float *)lds + wave * 16 * 128;
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < 8; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        stg[((r & 3) + 4 * (lane >> 5) + 8 * (r >> 2)) * SROW + j * 32 + (lane & 31)] = acc[i][j][r];
+      for (int r = 0; r < 4; ++r) stg[((lane >> 4) * 4 + r) * 128 + j * 16 + (lane & 15)] = acc[i][j][r];
     __syncthreads();
-    for (int row = 0; row < 32; ++row) {
-      const int m = wrow + i * 32 + row, n = wcol + lane * 2;
-      const float2 v = *(const float2 *)(stg + row * SROW + lane * 2);
+    for (int row = 0; row < 16; ++row) {
+      const int m = wrow + i * 16 + row, n = wcol + lane * 2;
+      const float2 v = *(const float2 *)(stg + row * 128 + lane * 2);
       if (m < M && n < N) epi_pair<T>(ep, m, n, v.x, v.y);
     }
     __syncthreads();
@@ -419,11 +422,11 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 // chip idle (the fp32 partials cost HBM traffic), and never below 1024 k per
 // split.  Returns the count the launch will use.
 int prefill_gemm_splits(int M, int N, int K) {
-  if (M <= 64 || K % (2 * PF_BK) != 0) return 1;
+  if (M <= 64 || K % PF_KQ != 0) return 1;
   const int64_t tiles = (int64_t)((M + PF_BM - 1) / PF_BM) * ((N + PF_BN - 1) / PF_BN);
-  int s = tiles < 64 ? 4 : tiles < 160 ? 2 : 1;
+  int s = tiles <= 64 ? 4 : tiles <= 160 ? 2 : 1;
   s = std::max(1, std::min(s, K / 1024));
-  const int kchunk = (K / s + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+  const int kchunk = (K / s + PF_KQ - 1) / PF_KQ * PF_KQ;
   return (K + kchunk - 1) / kchunk;
 }
 
@@ -509,8 +512,8 @@ int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K,
 int gemm_effective_splits(int M, int N, int K, int splits) {
   if (splits <= 1) return 1;
   if (M <= 64) return skinny_effective_splits(N, K, splits);
-  if (K % (2 * PF_BK) != 0) return 1;
-  const int kchunk = (K / splits + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+  if (K % PF_KQ != 0) return 1;
+  const int kchunk = (K / splits + PF_KQ - 1) / PF_KQ * PF_KQ;
   return (K + kchunk - 1) / kchunk;
 }
 
@@ -555,9 +558,9 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
     }
     return;
   }
-  if (K % (2 * PF_BK) == 0) {
+  if (K % PF_KQ == 0) {
     if (splits < 1 || part == nullptr) splits = 1;
-    int kchunk = (K / splits + 2 * PF_BK - 1) / (2 * PF_BK) * (2 * PF_BK);
+    int kchunk = (K / splits + PF_KQ - 1) / PF_KQ * PF_KQ;
     const int z = (K + kchunk - 1) / kchunk;
     dim3 grid((N + PF_BN - 1) / PF_BN, (M + PF_BM - 1) / PF_BM, z);
     launch_k(gemm_prefill_kernel<T>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
