@@ -251,7 +251,8 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
 // 16-bit decode attention on MFMA.  One wave owns one 64-position KV block:
 // S = Q K^T is four 16x16 tiles (query heads of the group padded to 16 rows,
 // positions as columns, head_dim as the contraction), the softmax is reduced
-// across the 16 lanes that hold a row, P goes through LDS into the A-operand
+// across the 16 lanes that hold a row (DPP lane moves, no LDS), P goes through
+// LDS into the A-operand
 // layout, and O = P V contracts over positions with V read from its
 // transposed [hd][64] block as 16-byte B fragments.  All K and V fragments
 // of the block are requested before any is used.
@@ -332,8 +333,7 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
       sacc[nt][i] = ok ? sacc[nt][i] * scale : -INFINITY;
       v = fmaxf(v, sacc[nt][i]);
     }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    v = row16_max(v);
     mx[i] = v;
     float t = 0.f;
 #pragma unroll
@@ -342,8 +342,7 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
       sacc[nt][i] = p;
       t += p;
     }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) t += __shfl_xor(t, o, 64);
+    t = row16_sum(t);
     sm[i] = t;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) pls[wave][4 * quad + i][nt * 16 + r16] = Act<T>::st(sacc[nt][i]);
@@ -502,8 +501,9 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(const T *__restrict__
 // transposed as [dim][key], rows padded so the 16-byte fragment reads of a
 // wave fall in distinct banks) with the next block prefetched into registers
 // while the current one is used.  S = Q K^T and O += P V are 16x16x32 MFMAs,
-// the softmax is online (running max and sum per row), and only the diagonal
-// block needs the causal mask.
+// the softmax is online (running max and sum per row, reduced across the 16
+// lanes of a row by DPP lane moves), and only the diagonal block needs the
+// causal mask.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void prefill_attn_mfma_kernel(const T *__restrict__ q, T *__restrict__ out,
                                                                 const int32_t *seq_start, const int32_t *seq_slot,
@@ -604,8 +604,7 @@ __global__ __launch_bounds__(256) void prefill_attn_mfma_kernel(const T *__restr
         sacc[nt][i] = ok ? sacc[nt][i] * scale : -INFINITY;
         mx = fmaxf(mx, sacc[nt][i]);
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      mx = row16_max(mx);
       // rows past the sequence end see no valid key: keep them finite
       const float mref = (mx == -INFINITY) ? 0.f : mx;
       const float corr = __expf(mrow[i] - mref);
@@ -616,8 +615,7 @@ __global__ __launch_bounds__(256) void prefill_attn_mfma_kernel(const T *__restr
         sacc[nt][i] = p;
         t += p;
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) t += __shfl_xor(t, o, 64);
+      t = row16_sum(t);
       lrow[i] = lrow[i] * corr + t;
       mrow[i] = mx;
 #pragma unroll

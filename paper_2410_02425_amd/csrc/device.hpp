@@ -95,6 +95,39 @@ __device__ __forceinline__ int64_t kv_block_base(const KVCache &kv, int layer, i
   return (((int64_t)layer * kv.n_blocks + blk) * kv.n_kv_heads + h) * (int64_t)KV_BLOCK * kv.head_dim;
 }
 
+// Max / sum over the 16 lanes of a DPP row (lanes 16r .. 16r+15), the result
+// in every lane of the row, in registers: swap within quads (xor 1, xor 2),
+// then combine mirrored half-rows and mirrored rows.  Each step combines two
+// equal partial results in either order, so all lanes end with the same value.
+template <typename F>
+__device__ __forceinline__ float row16_reduce(float v, F op) {
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));  // quad_perm 1,0,3,2
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));  // quad_perm 2,3,0,1
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false))); // row_half_mirror
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false))); // row_mirror
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  return row16_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  return row16_reduce(v, [](float a, float b) { return a + b; });
+}
+
+// 16 bytes per lane from global memory straight into LDS (gfx950's
+// global_load_lds_dwordx4): lane l's bytes land at LDS byte address
+// `lds` + 16 l, `lds` wave-uniform.  The load counts on vmcnt like any vector
+// load but is invisible to the compiler's wait-count tracking: callers wait
+// for it explicitly (s_waitcnt vmcnt) before a barrier and reading the data.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory", "m0");
+}
+
+// LDS byte address of a __shared__ object (for dma16).
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char *)p;
+}
+
 // Applies the epilogue to output columns (n, n+1) of row m, n even.
 template <typename T>
 __device__ __forceinline__ void epi_pair(const Epi &ep, int m, int n, float v0, float v1) {

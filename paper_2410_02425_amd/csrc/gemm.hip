@@ -302,13 +302,6 @@ constexpr int PF_KQ = 128;                          // K granularity of a split
 constexpr int PF_ABYTES = PF_BM * PF_BK * 2;        // activation bytes per stage
 constexpr int PF_SBYTES = (PF_BM + PF_BN) * PF_BK * 2;  // bytes per stage buffer
 
-// 16 bytes per lane from global memory into LDS at `lds` (wave-uniform byte
-// address) + 16 x lane.  The load is invisible to the compiler's wait-count
-// tracking; the prefill kernel waits for it explicitly.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory", "m0");
-}
-
 template <typename T>
 __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
@@ -322,7 +315,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   const int nk = (ke - kb) / PF_BK;
   const int64_t wkt = wpack_kt(K);
   const int nsl = (N + WT_ROWS - 1) / WT_ROWS;
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)lds;
+  const uint32_t lds0 = lds_addr(lds);
 
   // this wave's share of a stage: two 1 KB blocks of activations (16 rows
   // each) and two weight tiles
