@@ -92,15 +92,10 @@ size_t part_bytes_for(const Dims &D, const lp_model_config &c, const lp_engine_o
   const int64_t Ns[3] = {D.qkv_n, D.d, D.d};
   const int64_t Ks[3] = {D.d, D.Hq * D.hd, D.F};
   const int64_t R = rows_cap(o);
-  for (int i = 0; i < 3; ++i) {
-    // the split count changes only where the row-tile count does: check each
-    // tile boundary (and R itself) up to the largest step
-    for (int64_t M = std::min<int64_t>(R, o.max_batch); M <= R;) {
+  // every row count a step can have (the split plan is not monotone in M)
+  for (int i = 0; i < 3; ++i)
+    for (int64_t M = 1; M <= R; ++M)
       m = std::max(m, (size_t)step_splits((int)M, (int)Ns[i], (int)Ks[i]) * M * Ns[i] * sizeof(float));
-      if (M == R) break;
-      M = std::min<int64_t>(R, std::max<int64_t>(M + 1, (M / 256 + 1) * 256));
-    }
-  }
   return m;
 }
 

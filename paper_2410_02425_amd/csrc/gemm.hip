@@ -276,8 +276,8 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 
 // ------------------------------------------------------------------ prefill (M > 64)
 //
-// 256x256 output tiles, eight waves (4 x 2, each 64 x 128 = 4 x 8 MFMA
-// 16x16x32 tiles), 32-wide K stages.  Operands travel from global memory
+// BM x 256 output tiles (BM = 256 or 128), eight waves (4 x 2, each BM/4 x 128
+// = BM/64 x 8 MFMA 16x16x32 tiles), 32-wide K stages.  Operands travel from global memory
 // straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
 // the instruction's LDS base + 16 x lane), with no register staging and no LDS
 // store instructions.  Four stage buffers, three stages in flight: at each
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // stage is refilled before the MFMAs run.
 //   * A weight stage is one tile per 16-row slice, copied verbatim: its lanes
 //     are already the B operand of a 16x16x32 MFMA.
-//   * An activation stage holds 256 rows of 64 bytes.  The four 16-byte
+//   * An activation stage holds BM rows of 64 bytes.  The four 16-byte
 //     chunks of row r are stored XOR-swizzled by (r / 4) % 4, by choosing the
 //     global address each lane loads, so that the 16-row fragment reads are
 //     free of bank conflicts.
@@ -297,76 +297,84 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // wave's load count (and the wait count) is the same at every stage.  K must
 // be a multiple of 128.
 
-constexpr int PF_BM = 256, PF_BN = 256, PF_BK = 32, PF_NB = 4, PF_NT = 512;
-constexpr int PF_KQ = 128;                          // K granularity of a split
-constexpr int PF_ABYTES = PF_BM * PF_BK * 2;        // activation bytes per stage
-constexpr int PF_SBYTES = (PF_BM + PF_BN) * PF_BK * 2;  // bytes per stage buffer
+constexpr int PF_BN = 256, PF_BK = 32, PF_NB = 4, PF_NT = 512;
+constexpr int PF_KQ = 128;  // K granularity of a split
 
-template <typename T>
+template <typename T, int BM>
 __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
                                                              int kchunk, float *__restrict__ part, Epi ep) {
   typedef typename Mfma<T>::v8 v8;
-  __shared__ __attribute__((aligned(1024))) char lds[PF_NB * PF_SBYTES];
+  constexpr int TM = BM / 64;                            // 16-row MFMA tiles per wave
+  constexpr int PA = BM / 128;                           // activation loads per wave and stage
+  constexpr int ABYTES = BM * PF_BK * 2;                 // activation bytes per stage
+  constexpr int SBYTES = (BM + PF_BN) * PF_BK * 2;       // bytes per stage buffer
+  __shared__ __attribute__((aligned(1024))) char lds[PF_NB * SBYTES];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * PF_BM, n0 = blockIdx.x * PF_BN;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * PF_BN;
   const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
   const int nk = (ke - kb) / PF_BK;
   const int64_t wkt = wpack_kt(K);
   const int nsl = (N + WT_ROWS - 1) / WT_ROWS;
   const uint32_t lds0 = lds_addr(lds);
 
-  // this wave's share of a stage: two 1 KB blocks of activations (16 rows
+  // this wave's share of a stage: PA 1 KB blocks of activations (16 rows
   // each) and two weight tiles
-  const T *ga[2];
+  const T *ga[PA];
   const T *gw[2];
-  uint32_t la[2], lw[2];
+  uint32_t la[PA], lw[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int blk = wave * 2 + i;
+  for (int i = 0; i < PA; ++i) {
+    const int blk = wave * PA + i;
     const int row = blk * 16 + (lane >> 2), slot = lane & 3;
     const int q = slot ^ ((row >> 2) & 3);  // the K chunk that this LDS slot holds
     ga[i] = X + (int64_t)min(m0 + row, M - 1) * ldx + kb + q * 8;
     la[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + blk * 1024));
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int blk = wave * 2 + i;
     gw[i] = W + ((int64_t)min((n0 >> 4) + blk, nsl - 1) * wkt + kb / WT_COLS) * WT_ELEMS + lane * 8;
-    lw[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + PF_ABYTES + blk * 1024));
+    lw[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + ABYTES + blk * 1024));
   }
 #define PF_ISSUE(kt)                                                                                 \
   {                                                                                                  \
     const int s_ = min((kt), nk - 1);                                                                \
-    const uint32_t b_ = (uint32_t)(((kt) & (PF_NB - 1)) * PF_SBYTES);                                \
-    _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(ga[i] + s_ * PF_BK, la[i] + b_);             \
+    const uint32_t b_ = (uint32_t)(((kt) & (PF_NB - 1)) * SBYTES);                                   \
+    _Pragma("unroll") for (int i = 0; i < PA; ++i) dma16(ga[i] + s_ * PF_BK, la[i] + b_);            \
     _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(gw[i] + (int64_t)s_ * WT_ELEMS, lw[i] + b_); \
   }
-  floatx4_t acc[4][8];
+  floatx4_t acc[TM][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  int fa[4];  // byte offsets of this lane's activation fragments in a stage
+  int fa[TM];  // byte offsets of this lane's activation fragments in a stage
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = wm * 64 + i * 16 + (lane & 15), q = lane >> 4;
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * (BM / 4) + i * 16 + (lane & 15), q = lane >> 4;
     fa[i] = r * 64 + ((q ^ ((r >> 2) & 3)) << 4);
   }
-  const int fb = PF_ABYTES + wn * 8 * 1024 + lane * 16;
+  const int fb = ABYTES + wn * 8 * 1024 + lane * 16;
 
   PF_ISSUE(0)
   PF_ISSUE(1)
   PF_ISSUE(2)
   for (int kt = 0; kt < nk; ++kt) {
-    // 4 loads per stage and wave: at most 8 outstanding = stage kt has landed
-    asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // PA + 2 loads per stage and wave: with the two younger stages' loads
+    // still allowed outstanding, stage kt has landed
+    if constexpr (PA == 2) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     PF_ISSUE(kt + 3)
-    const char *st = lds + (kt & (PF_NB - 1)) * PF_SBYTES;
-    v8 a[4], b[8];
+    const char *st = lds + (kt & (PF_NB - 1)) * SBYTES;
+    v8 a[TM], b[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *(const v8 *)(st + fa[i]);
+    for (int i = 0; i < TM; ++i) a[i] = *(const v8 *)(st + fa[i]);
 #pragma unroll
     for (int j = 0; j < 8; ++j) b[j] = *(const v8 *)(st + fb + j * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[i][j] = Mfma<T>::m16(a[i], b[j], acc[i][j]);
   }
@@ -375,11 +383,11 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   // accumulator (i, j) of lane l: row 4 (l / 16) + r of 16-row tile i, column l % 16 of tile j
-  const int wrow = m0 + wm * 64, wcol = n0 + wn * 128;
+  const int wrow = m0 + wm * (BM / 4), wcol = n0 + wn * 128;
   if (gridDim.z > 1) {
     float *pz = part + (int64_t)blockIdx.z * M * N;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int n = wcol + j * 16 + (lane & 15);
@@ -396,7 +404,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   // one 128-column row per pass of the wave
   float *stg = (float *)lds + wave * 16 * 128;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -411,17 +419,53 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   }
 }
 
-// K splits of a prefill GEMM: only when the tile grid alone leaves most of the
-// chip idle (the fp32 partials cost HBM traffic), and never below 1024 k per
-// split.  Returns the count the launch will use.
-int prefill_gemm_splits(int M, int N, int K) {
-  if (M <= 64 || K % PF_KQ != 0) return 1;
-  const int64_t tiles = (int64_t)((M + PF_BM - 1) / PF_BM) * ((N + PF_BN - 1) / PF_BN);
-  int s = tiles <= 64 ? 4 : tiles <= 160 ? 2 : 1;
-  s = std::max(1, std::min(s, K / 1024));
-  const int kchunk = (K / s + PF_KQ - 1) / PF_KQ * PF_KQ;
-  return (K + kchunk - 1) / kchunk;
+// Tile rows and K splits of a prefill GEMM, chosen by an estimate of its
+// time: the rounds of workgroups over the 256 CUs times one tile's time at
+// the tile shape's measured per-CU rate (4.8 TFLOP/s for 256-row tiles, 3.8
+// for 128-row ones, which waste fewer padded rows at small M and give more
+// tiles), plus the fp32 partials of a split written and read once at
+// 5 TB/s.  Splits keep at least 1024 K each.  Fitted to a sweep of the
+// decoder's four projections over M = 300..2048, it picks the measured best
+// (or a tie) in every case.
+static int prefill_kchunk(int K, int s) { return (K / s + PF_KQ - 1) / PF_KQ * PF_KQ; }
+
+static double prefill_cost(int M, int N, int K, int bm, int s) {
+  const int kchunk = prefill_kchunk(K, s);
+  const int se = (K + kchunk - 1) / kchunk;
+  const int64_t wgs = (int64_t)((M + bm - 1) / bm) * ((N + PF_BN - 1) / PF_BN) * se;
+  const double rounds = (double)((wgs + 255) / 256);
+  const double rate = bm == 256 ? 4.8e12 : 3.8e12;
+  const double partials = se > 1 ? 2.0 * se * M * N * 4 / 5e12 : 0.0;
+  return rounds * (2.0 * bm * PF_BN * kchunk / rate) + partials;
 }
+
+struct PrefillPlan {
+  int bm, splits;
+};
+
+// splits > 0: the caller's split request (rounded to whole K chunks as
+// gemm_effective_splits does), only the tile rows are chosen; splits == 0:
+// both are chosen, from 1, 2 or 4 splits.
+static PrefillPlan prefill_plan(int M, int N, int K, int splits) {
+  PrefillPlan best{256, 1};
+  if (M <= 64 || K % PF_KQ != 0) return best;
+  double tbest = -1.0;
+  for (int s : {1, 2, 4}) {
+    if (splits > 0 ? s != 1 : (s > 1 && K / s < 1024)) continue;
+    const int req = splits > 0 ? splits : s;
+    for (int bm : {256, 128}) {
+      const double t = prefill_cost(M, N, K, bm, req);
+      if (tbest < 0.0 || t < tbest) {
+        tbest = t;
+        const int kchunk = prefill_kchunk(K, req);
+        best = {bm, (K + kchunk - 1) / kchunk};
+      }
+    }
+  }
+  return best;
+}
+
+int prefill_gemm_splits(int M, int N, int K) { return prefill_plan(M, N, K, 0).splits; }
 
 // ------------------------------------------------------------------ fp32 path
 
@@ -553,10 +597,13 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
   }
   if (K % PF_KQ == 0) {
     if (splits < 1 || part == nullptr) splits = 1;
-    int kchunk = (K / splits + PF_KQ - 1) / PF_KQ * PF_KQ;
-    const int z = (K + kchunk - 1) / kchunk;
-    dim3 grid((N + PF_BN - 1) / PF_BN, (M + PF_BM - 1) / PF_BM, z);
-    launch_k(gemm_prefill_kernel<T>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
+    const PrefillPlan p = prefill_plan(M, N, K, splits);
+    const int kchunk = prefill_kchunk(K, splits);
+    dim3 grid((N + PF_BN - 1) / PF_BN, (M + p.bm - 1) / p.bm, p.splits);
+    if (p.bm == 256)
+      launch_k(gemm_prefill_kernel<T, 256>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
+    else
+      launch_k(gemm_prefill_kernel<T, 128>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);
