@@ -153,7 +153,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
       for (int r = 0; r < 4; ++r) {
         const int m = i * 16 + (lane >> 4) * 4 + r;
         const float v = acc[i][j][r];
-        const float other = __shfl_xor(v, 1, 64);
+        const float other = lane_xor1(v);
         if (split) {
           if (m < M && n < N) part[((int64_t)blockIdx.y * M + m) * N + n] = v;
         } else if ((lane & 1) == 0 && m < M && n < N) {
