@@ -254,8 +254,8 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
 // across the 16 lanes that hold a row (DPP lane moves, no LDS), P goes through
 // LDS into the A-operand
 // layout, and O = P V contracts over positions with V read from its
-// transposed [hd][64] block as 16-byte B fragments.  All K and V fragments
-// of the block are requested before any is used.
+// transposed [hd][64] block as 16-byte B fragments.  All K fragments of the
+// block are requested before any is used, then all V fragments.
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restrict__ q, RowMeta rows, KVCache kv,
                                                                int layer, int M, int n_heads, int max_ctx,
@@ -282,24 +282,37 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) qa[ks] = (r16 < G) ? load8<T>(qrow + ks * 32 + kq) : zero8<T>();
 
-  v8 kf[4][KS], vf[NT][2];
+  const int64_t base = nvalid > 0 ? kv_block_base(kv, layer, slot, blk_pos, g) : 0;
+  v8 kf[4][KS];
   if (nvalid > 0) {
-    const int64_t base = kv_block_base(kv, layer, slot, blk_pos, g);
     const T *kb = (const T *)kv.k + base;
-    const T *vb = (const T *)kv.v + base;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) vf[nt][kk] = load8<T>(vb + (nt * 16 + r16) * KV_BLOCK + kk * 32 + kq);
   } else {
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = zero8<T>();
+  }
+  floatx4_t sacc[4];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) {
+    sacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) sacc[nt] = Mfma<T>::m16(qa[ks], kf[nt][ks], sacc[nt]);
+  }
+  // V is requested once the K fragments are consumed: the registers K held
+  // take V, which keeps the kernel at three workgroups per CU
+  v8 vf[NT][2];
+  if (nvalid > 0) {
+    const T *vb = (const T *)kv.v + base;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) vf[nt][kk] = load8<T>(vb + (nt * 16 + r16) * KV_BLOCK + kk * 32 + kq);
+  } else {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) vf[nt][0] = vf[nt][1] = zero8<T>();
   }
@@ -312,14 +325,6 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (kk * 32 + kq + e >= nvalid) vf[nt][kk][e] = (typename Mfma<T>::v8){}[0];
-  }
-
-  floatx4_t sacc[4];
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    sacc[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) sacc[nt] = Mfma<T>::m16(qa[ks], kf[nt][ks], sacc[nt]);
   }
   // sacc[nt][i]: row (head) 4*quad + i, position nt*16 + r16
   const float scale = rsqrtf((float)HD);
