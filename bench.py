@@ -189,6 +189,9 @@ def main():
     ap.add_argument("--act", choices=["f16", "bf16"], default="f16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--step-log", default="",
+                    help="write the last timed run's steps (kind, rows, context sum, duration, decode "
+                         "algorithmic bytes) to this JSON file")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device 5 times (a plain copy kernel of known size, "
                          "the reference for the HBM byte counters)")
@@ -248,6 +251,12 @@ def main():
     prev_end = {i: (log[i - 1]["end_ns"] if i else 0) for i in range(len(log))}
     full_idx = [i for i, st in enumerate(log) if st["kind"] == "decode" and st["n_rows"] == wl.max_batch]
     full_ns = sum(log[i]["end_ns"] - prev_end[i] for i in full_idx)
+    if args.step_log:
+        with open(args.step_log, "w") as f:
+            json.dump([{"kind": st["kind"], "n_rows": st["n_rows"], "sum_ctx": st["sum_ctx"],
+                        "ns": st["end_ns"] - prev_end[i],
+                        "bytes": decode_step_bytes(shape, st["n_rows"], st["sum_ctx"])
+                        if st["kind"] == "decode" else None} for i, st in enumerate(log)], f)
     full_bytes = sum(decode_step_bytes(shape, log[i]["n_rows"], log[i]["sum_ctx"]) for i in full_idx)
     full_tokens = sum(log[i]["n_rows"] for i in full_idx)
     decode_gbs = full_bytes / full_ns if full_ns else 0.0

@@ -172,11 +172,21 @@ __global__ void gemm_finish_kernel(const float *__restrict__ part, int splits, i
   if (p >= (int64_t)M * half) return;
   const int m = (int)(p / half);
   const int n = (int)(p % half) * 2;
+  // partials are requested eight splits at a time before any is added, and
+  // added in split order
+  constexpr int U = 8;
   float v0 = 0.f, v1 = 0.f;
-  for (int s = 0; s < splits; ++s) {
-    const float2 q = *(const float2 *)(part + ((int64_t)s * M + m) * N + n);
-    v0 += q.x;
-    v1 += q.y;
+  for (int s0 = 0; s0 < splits; s0 += U) {
+    float2 q[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      q[u] = *(const float2 *)(part + ((int64_t)min(s0 + u, splits - 1) * M + m) * N + n);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < splits) {
+        v0 += q[u].x;
+        v1 += q[u].y;
+      }
   }
   epi_pair<T>(ep, m, n, v0, v1);
 }

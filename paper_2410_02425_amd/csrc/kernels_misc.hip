@@ -30,9 +30,9 @@ void launch_embed(const T *E, const int32_t *pool, const int32_t *tok_idx, const
 
 constexpr int NORM_V4 = 4;  // float4 per thread; the block has d / 16 threads (rounded to waves)
 
-// One workgroup per row.  The residual row and every split-K partial of it
-// are requested before any is summed (NP is the partial count), so a row costs
-// one memory latency rather than one per partial.
+// One workgroup per row.  The residual row, every split-K partial of it and
+// the gains are requested before any is used (NP is the partial count), so a
+// row costs one memory latency rather than one per partial.
 template <typename T, int NP>
 __global__ __launch_bounds__(512) void rmsnorm_kernel(float *x, const float *part, int64_t part_stride,
                                                        const int32_t *rows, const float *__restrict__ g,
@@ -43,13 +43,15 @@ __global__ __launch_bounds__(512) void rmsnorm_kernel(float *x, const float *par
   const int d4 = d >> 2;
   const int nt = blockDim.x;
   float4 *xr = (float4 *)(x + (int64_t)src * d);
-  float4 v[NORM_V4];
+  const float4 *g4 = (const float4 *)g;
+  float4 v[NORM_V4], gv[NORM_V4];
   float4 p[NP > 0 ? NP : 1][NORM_V4];
 #pragma unroll
   for (int e = 0; e < NORM_V4; ++e) {
     const int c = threadIdx.x + e * nt;
     if (c < d4) {
       v[e] = xr[c];
+      gv[e] = g4[c];
 #pragma unroll
       for (int s = 0; s < NP; ++s) p[s][e] = ((const float4 *)(part + s * part_stride + (int64_t)src * d))[c];
     }
@@ -77,12 +79,11 @@ __global__ __launch_bounds__(512) void rmsnorm_kernel(float *x, const float *par
   for (int w = 0; w < (nt >> 6); ++w) tot += red[w];
   const float r = rsqrtf(tot / (float)d + eps);
   T *yr = y + (int64_t)j * d;
-  const float4 *g4 = (const float4 *)g;
 #pragma unroll
   for (int e = 0; e < NORM_V4; ++e) {
     const int c = threadIdx.x + e * nt;
     if (c < d4) {
-      const float4 gg = g4[c];
+      const float4 gg = gv[e];
       yr[4 * c + 0] = Act<T>::st(v[e].x * r * gg.x);
       yr[4 * c + 1] = Act<T>::st(v[e].y * r * gg.y);
       yr[4 * c + 2] = Act<T>::st(v[e].z * r * gg.z);
