@@ -36,9 +36,10 @@ int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *
 /* The tiled weight layout of the 16-bit GEMMs (weights of Sec. II-A's
  * decoder, stored for the decode phase's weight stream).  A row-major [N x K]
  * matrix W (row n = output feature n, stride K, K % 8 == 0) becomes
- * ceil(N/16) * ceil(K/32) tiles of 16 rows x 32 columns, 1024 elements each;
- * tile (i, j) has index i * ceil(K/32) + j and holds rows 16i..16i+15,
- * columns 32j..32j+31, its element (r, c) at position
+ * ceil(N/16) * ceil(K/32) tiles of 16 rows x 32 columns, 512 elements (1 KB) each;
+ * tile (i, j) has index j * ceil(N/16) + i (the tiles of one 32-column step
+ * side by side) and holds rows 16i..16i+15, columns 32j..32j+31, its element
+ * (r, c) at position
  * 8 * (r + 16 * (c / 8)) + c % 8.  Rows >= N and columns >= K are zero.
  * lp_op_packed_weight_bytes gives the size (0 for other dtypes or
  * non-positive sizes); lp_op_pack_weight writes W_packed (device, that many

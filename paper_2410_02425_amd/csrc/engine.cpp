@@ -391,15 +391,18 @@ std::vector<TensorDesc> canonical(const Dims &D) {
   return t;
 }
 
-// Destination of canonical tensor i: byte offset of its row 0, row
-// permutation, whether it is a norm gain (fp32), and whether it is stored in
-// the tiled weight layout (every GEMM weight of a 16-bit model; the embedding
-// table stays row-major for the row gather).
+// Destination of canonical tensor i: row permutation, whether it is a norm
+// gain (fp32), and whether it is stored in the tiled weight layout (every GEMM
+// weight of a 16-bit model; the embedding table stays row-major for the row
+// gather).  Row-major: `off` is the byte offset of the tensor's row 0.  Tiled:
+// `off` is the byte offset of the whole fused matrix (fused_rows rows), whose
+// rows from row0 on are this tensor's (q, k and v share one matrix).
 struct Dest {
   size_t off;
   int perm;
   bool gain;
   bool packed;
+  int64_t row0 = 0, fused_rows = 0;
 };
 
 Dest dest_of(const lp_engine *e, int i) {
@@ -408,31 +411,32 @@ Dest dest_of(const lp_engine *e, int i) {
   if (i == 0) return {e->Ly.embed, PERM_NONE, false, false};
   const int last = 1 + 9 * D.L;
   if (i == last) return {e->Ly.final_norm, PERM_NONE, true, false};
-  if (i == last + 1) return {e->Ly.lm_head, PERM_NONE, false, pk};
+  if (i == last + 1) return {e->Ly.lm_head, PERM_NONE, false, pk, 0, D.V};
   const int l = (i - 1) / 9, j = (i - 1) % 9;
-  // q, k and v start at whole 16-row slices, so their tiles are contiguous
-  // ranges of the fused matrix in either layout
-  const size_t rowb = (size_t)(pk ? wpack_kt(D.d) * WT_COLS : D.d) * D.esz;
+  // q, k and v are rows [0, Hq hd), [Hq hd, (Hq + Hkv) hd) and the rest of
+  // one fused matrix
+  const int64_t qr = (int64_t)D.Hq * D.hd, kr = (int64_t)D.Hkv * D.hd;
+  const size_t rowb = (size_t)D.d * D.esz;
   switch (j) {
     case 0: return {e->Ly.attn_norm[l], PERM_NONE, true, false};
-    case 1: return {e->Ly.wqkv[l], PERM_ROPE, false, pk};
-    case 2: return {e->Ly.wqkv[l] + (size_t)D.Hq * D.hd * rowb, PERM_ROPE, false, pk};
-    case 3: return {e->Ly.wqkv[l] + (size_t)(D.Hq + D.Hkv) * D.hd * rowb, PERM_NONE, false, pk};
-    case 4: return {e->Ly.wo[l], PERM_NONE, false, pk};
+    case 1: return {e->Ly.wqkv[l], PERM_ROPE, false, pk, 0, D.qkv_n};
+    case 2: return {e->Ly.wqkv[l] + (pk ? 0 : qr * rowb), PERM_ROPE, false, pk, qr, D.qkv_n};
+    case 3: return {e->Ly.wqkv[l] + (pk ? 0 : (qr + kr) * rowb), PERM_NONE, false, pk, qr + kr, D.qkv_n};
+    case 4: return {e->Ly.wo[l], PERM_NONE, false, pk, 0, D.d};
     case 5: return {e->Ly.mlp_norm[l], PERM_NONE, true, false};
-    case 6: return {e->Ly.wgu[l], PERM_GATE, false, pk};
-    case 7: return {e->Ly.wgu[l], PERM_UP, false, pk};
-    default: return {e->Ly.wd[l], PERM_NONE, false, pk};
+    case 6: return {e->Ly.wgu[l], PERM_GATE, false, pk, 0, 2 * (int64_t)D.F};
+    case 7: return {e->Ly.wgu[l], PERM_UP, false, pk, 0, 2 * (int64_t)D.F};
+    default: return {e->Ly.wd[l], PERM_NONE, false, pk, 0, D.d};
   }
 }
 
 // Host-side packing of a row-major rows x K matrix of 16-bit values into the
 // tiled weight layout (K % 8 == 0; padding zeroed).
 std::vector<uint16_t> pack_tiles(const uint16_t *src, int64_t rows, int64_t K) {
-  const int64_t kt = wpack_kt(K);
+  const int64_t ns = wpack_ns(rows);
   std::vector<uint16_t> out((size_t)wpack_elems(rows, K), 0);
   for (int64_t n = 0; n < rows; ++n)
-    for (int64_t k = 0; k < K; k += 8) memcpy(&out[(size_t)wpack_off(n, k, kt)], src + n * K + k, 16);
+    for (int64_t k = 0; k < K; k += 8) memcpy(&out[(size_t)wpack_off(n, k, ns)], src + n * K + k, 16);
   return out;
 }
 
@@ -519,8 +523,18 @@ extern "C" int lp_load_weights(lp_engine *e, const void *blob, size_t bytes) {
         if (ds.perm == PERM_GATE)
           memcpy(tmp.data() + perm_row(PERM_UP, r, D.hd) * rowb, src + (t.rows + r) * rowb, rowb);
       }
+      // the tensor's tiles of one K step are one run of its slices inside
+      // the fused matrix's K step: one strided copy places them all
       const std::vector<uint16_t> pk = pack_tiles((const uint16_t *)tmp.data(), out_rows, t.cols);
-      HIPCHK(e, hipMemcpy(e->arena + ds.off, pk.data(), pk.size() * 2, hipMemcpyHostToDevice));
+      const int64_t ns = wpack_ns(out_rows), fused_ns = wpack_ns(ds.fused_rows);
+      if (ds.row0 % WT_ROWS || (ds.row0 + out_rows < ds.fused_rows && out_rows % WT_ROWS) ||
+          ds.row0 / WT_ROWS + ns > fused_ns) {
+        e->err = "a fused weight piece does not start and end at whole 16-row slices";
+        return LP_EINVAL;
+      }
+      const size_t tile_b = (size_t)WT_ELEMS * 2;
+      HIPCHK(e, hipMemcpy2D(e->arena + ds.off + (size_t)(ds.row0 / WT_ROWS) * tile_b, fused_ns * tile_b,
+                            pk.data(), ns * tile_b, ns * tile_b, wpack_kt(t.cols), hipMemcpyHostToDevice));
     } else if (ds.perm == PERM_NONE) {
       HIPCHK(e, hipMemcpy(e->arena + ds.off, src, rowb * t.rows, hipMemcpyHostToDevice));
     } else {
@@ -556,13 +570,13 @@ extern "C" int lp_init_weights_random(lp_engine *e, uint64_t seed, float stdv) {
       launch_fill_f32((float *)(e->arena + ds.off), t.cols, 1.0f, e->stream);
     } else if (D.act == ACT_F16) {
       launch_init_weight<f16_t>((f16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                ds.perm, D.hd, true, ds.packed, e->stream);
+                                ds.perm, D.hd, true, ds.packed, ds.row0, ds.fused_rows, e->stream);
     } else if (D.act == ACT_BF16) {
       launch_init_weight<bf16_t>((bf16_t *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                 ds.perm, D.hd, false, ds.packed, e->stream);
+                                 ds.perm, D.hd, false, ds.packed, ds.row0, ds.fused_rows, e->stream);
     } else {
       launch_init_weight<float>((float *)(e->arena + ds.off), k0, k1, (uint32_t)i, t.rows, t.cols, stdv,
-                                ds.perm, D.hd, false, false, e->stream);
+                                ds.perm, D.hd, false, false, 0, 0, e->stream);
     }
   }
   HIPCHK(e, hipGetLastError());

@@ -32,9 +32,9 @@ namespace lp {
 // cost: each wave owns NS 16-row slices of W and streams them over the
 // workgroup's K range, one sub-chunk (KSUB 32-wide k-steps, one weight tile
 // each) ahead of the MFMAs.  With the tiled layout every weight load is 1 KB
-// of contiguous memory and a slice is read front to back, which keeps the
-// HBM pages that the concurrent waves stream open far longer than 64-byte
-// pieces of 16 separate rows would.
+// of contiguous memory, and since the tiles of one K step lie side by side
+// across the slices, all workgroups, starting together at their K range's
+// first sub-chunk, sweep one compact region of the matrix.
 // The activations of a sub-chunk are staged once per workgroup into LDS in
 // MFMA-fragment order (one 1 KB block per (k-step, m-tile), lane-major), so
 // they never occupy the vector-memory counter the weight prefetch waits on.
@@ -42,8 +42,6 @@ namespace lp {
 // past the end re-read the last sub-chunk, so the compiler's wait counts stay
 // exact.  Columns of the workgroup's chunk beyond K are zeroed in LDS; the
 // weight loads there read valid neighbouring memory and meet those zeros.
-// Each workgroup rotates its starting sub-chunk so that concurrent
-// workgroups spread over the K range.
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -64,15 +62,15 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
   const int n0 = (blockIdx.x * NW + wave) * NS * 16;
   const int kbeg = blockIdx.y * kchunk, kend = min(K, kbeg + kchunk);
   const int nsub = ((kend - kbeg + 2 * KC - 1) / (2 * KC)) * 2;
-  const int rot = (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nsub);
-#define SK_SC(c) (kbeg + (((c) + rot) % nsub) * KC)
+#define SK_SC(c) (kbeg + (c) * KC)
   const int klast = SK_SC(nsub - 1);
 
   const int64_t wkt = wpack_kt(K);
   const int nsl = (N + WT_ROWS - 1) / WT_ROWS;  // 16-row slices of W
   const T *wrow[NS];
 #pragma unroll
-  for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min((n0 >> 4) + j, nsl - 1) * wkt * WT_ELEMS + lane * 8;
+  for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min((n0 >> 4) + j, nsl - 1) * WT_ELEMS + lane * 8;
+  const int64_t wstep = (int64_t)nsl * WT_ELEMS;  // one tile further along K
   const T *xsrc[XF];
   int xk[XF];
 #pragma unroll
@@ -102,7 +100,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
 #define SK_WLOAD(WB, kb)                                                                        \
   _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
     const int64_t t = min((int64_t)((kb) >> 5) + ks, wkt - 1);                                  \
-    _Pragma("unroll") for (int j = 0; j < NS; ++j) WB[ks][j] = load8<T>(wrow[j] + t * WT_ELEMS); \
+    _Pragma("unroll") for (int j = 0; j < NS; ++j) WB[ks][j] = load8<T>(wrow[j] + t * wstep);    \
   }
 #define SK_MMA(WB, XS)                                                                          \
   _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
@@ -213,7 +211,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * BG_BM, n0 = blockIdx.x * BG_BN;
-  const int64_t wkt = wpack_kt(K);
+  const int64_t wns = wpack_ns(N);
 
   // global -> register staging: each thread moves 4 chunks of 16 B for A and B
   uint4 ra[4], rb[4];
@@ -223,7 +221,7 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
     const int row = idx >> 3, kk = (k0) + (idx & 7) * 8;                                        \
     const int m = m0 + row, n = n0 + row;                                                       \
     ra[c] = (m < M && kk < K) ? *(const uint4 *)(X + (int64_t)m * ldx + kk) : make_uint4(0, 0, 0, 0); \
-    rb[c] = (n < N && kk < K) ? *(const uint4 *)(W + wpack_off(n, kk, wkt)) : make_uint4(0, 0, 0, 0); \
+    rb[c] = (n < N && kk < K) ? *(const uint4 *)(W + wpack_off(n, kk, wns)) : make_uint4(0, 0, 0, 0); \
   }
   floatx16_t acc[2][2];
 #pragma unroll
@@ -296,7 +294,8 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // makes every wave's loads visible, and the buffer freed by the previous
 // stage is refilled before the MFMAs run.
 //   * A weight stage is one tile per 16-row slice, copied verbatim: its lanes
-//     are already the B operand of a 16x16x32 MFMA.
+//     are already the B operand of a 16x16x32 MFMA, and the 16 tiles of a
+//     stage lie side by side in memory.
 //   * An activation stage holds BM rows of 64 bytes.  The four 16-byte
 //     chunks of row r are stored XOR-swizzled by (r / 4) % 4, by choosing the
 //     global address each lane loads, so that the 16-row fragment reads are
@@ -325,8 +324,8 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * PF_BN;
   const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
   const int nk = (ke - kb) / PF_BK;
-  const int64_t wkt = wpack_kt(K);
   const int nsl = (N + WT_ROWS - 1) / WT_ROWS;
+  const int64_t wstep = (int64_t)nsl * WT_ELEMS;  // one tile further along K
   const uint32_t lds0 = lds_addr(lds);
 
   // this wave's share of a stage: PA 1 KB blocks of activations (16 rows
@@ -345,7 +344,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int blk = wave * 2 + i;
-    gw[i] = W + ((int64_t)min((n0 >> 4) + blk, nsl - 1) * wkt + kb / WT_COLS) * WT_ELEMS + lane * 8;
+    gw[i] = W + ((int64_t)(kb / WT_COLS) * nsl + min((n0 >> 4) + blk, nsl - 1)) * WT_ELEMS + lane * 8;
     lw[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + ABYTES + blk * 1024));
   }
 #define PF_ISSUE(kt)                                                                                 \
@@ -353,7 +352,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
     const int s_ = min((kt), nk - 1);                                                                \
     const uint32_t b_ = (uint32_t)(((kt) & (PF_NB - 1)) * SBYTES);                                   \
     _Pragma("unroll") for (int i = 0; i < PA; ++i) dma16(ga[i] + s_ * PF_BK, la[i] + b_);            \
-    _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(gw[i] + (int64_t)s_ * WT_ELEMS, lw[i] + b_); \
+    _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(gw[i] + s_ * wstep, lw[i] + b_);             \
   }
   floatx4_t acc[TM][8];
 #pragma unroll
@@ -647,9 +646,9 @@ template <typename T>
 __global__ void wpack_kernel(const T *__restrict__ src, T *__restrict__ dst, int N, int K, int64_t pieces) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= pieces) return;
-  const int64_t kt = wpack_kt(K), t = p >> 6;
+  const int64_t ns = wpack_ns(N), t = p >> 6;
   const int l = (int)(p & 63);
-  const int64_t n = (t / kt) * WT_ROWS + (l & 15), k = (t % kt) * WT_COLS + (l >> 4) * 8;
+  const int64_t n = (t % ns) * WT_ROWS + (l & 15), k = (t / ns) * WT_COLS + (l >> 4) * 8;
   uint4 v = make_uint4(0, 0, 0, 0);
   if (n < N && k < K) v = *(const uint4 *)(src + n * K + k);
   *(uint4 *)(dst + p * 8) = v;

@@ -15,20 +15,20 @@ typedef _Float16 f16_t;
 // Tiled layout of 16-bit weight matrices, read by every 16-bit GEMM kernel.
 // An [N x K] matrix (row n is output feature n, K its inputs) is cut into
 // tiles of 16 rows x 32 columns, 1 KB each.  Tile (i, j) holds rows
-// 16i..16i+15 and columns 32j..32j+31 and has index i * ceil(K/32) + j, so
-// the tiles of one 16-row slice follow each other along K.  Inside a tile the
-// 8 elements of lane l = r + 16q (r < 16, q < 4) are row 16i + r, columns
-// 32j + 8q .. 32j + 8q + 7: the B operand of a 16x16x32 MFMA, so a wave reads
-// a tile with one contiguous 1 KB load and streams a slice front to back.
+// 16i..16i+15 and columns 32j..32j+31 and has index j * ceil(N/16) + i: the
+// tiles of one K step follow each other across the slices, so waves that
+// stream their slices side by side in K read one compact, moving region of
+// the matrix.  Inside a tile the 8 elements of lane l = r + 16q (r < 16,
+// q < 4) are row 16i + r, columns 32j + 8q .. 32j + 8q + 7: the B operand of
+// a 16x16x32 MFMA, so a wave reads a tile with one contiguous 1 KB load.
 // Rows past N and columns past K are zero.
 constexpr int WT_ROWS = 16, WT_COLS = 32, WT_ELEMS = WT_ROWS * WT_COLS;
 __host__ __device__ inline int64_t wpack_kt(int64_t K) { return (K + WT_COLS - 1) / WT_COLS; }
-__host__ __device__ inline int64_t wpack_elems(int64_t N, int64_t K) {
-  return (N + WT_ROWS - 1) / WT_ROWS * wpack_kt(K) * WT_ELEMS;
-}
-// Element offset of (n, k) for a matrix with kt = wpack_kt(K) tiles along K.
-__host__ __device__ inline int64_t wpack_off(int64_t n, int64_t k, int64_t kt) {
-  return ((n >> 4) * kt + (k >> 5)) * WT_ELEMS + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+__host__ __device__ inline int64_t wpack_ns(int64_t N) { return (N + WT_ROWS - 1) / WT_ROWS; }
+__host__ __device__ inline int64_t wpack_elems(int64_t N, int64_t K) { return wpack_ns(N) * wpack_kt(K) * WT_ELEMS; }
+// Element offset of (n, k) for a matrix with ns = wpack_ns(N) 16-row slices.
+__host__ __device__ inline int64_t wpack_off(int64_t n, int64_t k, int64_t ns) {
+  return ((k >> 5) * ns + (n >> 4)) * WT_ELEMS + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
 }
 
 // Where the rows of a step read their token and write their results.
@@ -156,10 +156,13 @@ void launch_sample(const float *logits, int64_t ld, int M, int V, const SamplePa
 // tiled weight layout of a cols-wide matrix.  `bf16_values`: round each value
 // to bf16 first (a bf16 model held in fp16 storage keeps its exact values).
 enum RowPerm : int { PERM_NONE = 0, PERM_ROPE = 1, PERM_GATE = 2, PERM_UP = 3 };
+// packed: dst is the tiled matrix of fused_rows rows that holds this tensor's
+// (permuted) rows from row0 on; otherwise dst is the tensor's row 0 of a
+// row-major matrix.
 template <typename T>
 void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
                         int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, bool packed,
-                        hipStream_t s);
+                        int64_t row0, int64_t fused_rows, hipStream_t s);
 void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s);
 
 }  // namespace lp

@@ -392,7 +392,8 @@ void launch_sample(const float *logits, int64_t ld, int M, int V, const SamplePa
 
 template <typename T>
 __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t tid, int64_t rows,
-                                   int64_t cols, float stdv, int perm, int hd, bool bf16_values, bool packed) {
+                                   int64_t cols, float stdv, int perm, int hd, bool bf16_values, bool packed,
+                                   int64_t row0, int64_t fused_ns) {
   const int64_t n = rows * cols;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (int64_t)gridDim.x * blockDim.x) {
@@ -413,18 +414,19 @@ __global__ void init_weight_kernel(T *dst, uint32_t k0, uint32_t k1, uint32_t ti
     } else if (perm == PERM_UP) {
       dr = 2 * r + 1;
     }
-    dst[packed ? wpack_off(dr, col, wpack_kt(cols)) : dr * cols + col] = Act<T>::st(v);
+    dst[packed ? wpack_off(row0 + dr, col, fused_ns) : dr * cols + col] = Act<T>::st(v);
   }
 }
 
 template <typename T>
 void launch_init_weight(T *dst, uint32_t k0, uint32_t k1, uint32_t tensor_id, int64_t rows,
                         int64_t cols, float stdv, int perm, int head_dim, bool bf16_values, bool packed,
-                        hipStream_t s) {
+                        int64_t row0, int64_t fused_rows, hipStream_t s) {
   const int64_t n = rows * cols;
   const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
-  init_weight_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(dst, k0, k1, tensor_id, rows, cols, stdv,
-                                                        perm, head_dim, bf16_values, packed);
+  init_weight_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(dst, k0, k1, tensor_id, rows, cols, stdv, perm,
+                                                        head_dim, bf16_values, packed, row0,
+                                                        wpack_ns(fused_rows));
 }
 
 __global__ void fill_f32_kernel(float *dst, int64_t n, float v) {
@@ -444,7 +446,7 @@ void launch_fill_f32(float *dst, int64_t n, float v, hipStream_t s) {
   template void launch_rmsnorm<T>(float *, const float *, int, int64_t, const int32_t *,          \
                                   const float *, T *, int, int, float, hipStream_t);              \
   template void launch_init_weight<T>(T *, uint32_t, uint32_t, uint32_t, int64_t, int64_t, float, \
-                                      int, int, bool, bool, hipStream_t);
+                                      int, int, bool, bool, int64_t, int64_t, hipStream_t);
 INST(float)
 INST(bf16_t)
 INST(f16_t)

@@ -171,13 +171,13 @@ extern "C" int lp_op_init_weight(int32_t dtype, void *dst, uint64_t seed, int32_
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
     launch_init_weight<bf16_t>((bf16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
-                               cols, stdv, PERM_NONE, 0, false, false, s);
+                               cols, stdv, PERM_NONE, 0, false, false, 0, 0, s);
   else if (dtype == LP_F16)
     launch_init_weight<f16_t>((f16_t *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows,
-                              cols, stdv, PERM_NONE, 0, true, false, s);
+                              cols, stdv, PERM_NONE, 0, true, false, 0, 0, s);
   else if (dtype == LP_F32)
     launch_init_weight<float>((float *)dst, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)tensor_id, rows, cols,
-                              stdv, PERM_NONE, 0, false, false, s);
+                              stdv, PERM_NONE, 0, false, false, 0, 0, s);
   else
     OPCHK(false, "init_weight: dtype");
   return op_status();

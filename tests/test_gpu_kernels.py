@@ -54,7 +54,7 @@ def packed(Wd):
 
 def tile_layout_reference(W):
     """The tiled layout written out from its definition: tiles of 16 rows x 32
-    columns, tile (i, j) at index i * ceil(K/32) + j, element (r, c) of a tile
+    columns, tile (i, j) at index j * ceil(N/16) + i, element (r, c) of a tile
     at 8 * (r + 16 * (c // 8)) + c % 8, zeros past N and K."""
     N, K = W.shape
     nt, kt = -(-N // 16), -(-K // 32)
@@ -64,7 +64,7 @@ def tile_layout_reference(W):
     for i in range(nt):
         for j in range(kt):
             tile = full[16 * i:16 * i + 16, 32 * j:32 * j + 32]
-            base = (i * kt + j) * 512
+            base = (j * nt + i) * 512
             for r in range(16):
                 for c in range(32):
                     out[base + 8 * (r + 16 * (c // 8)) + c % 8] = tile[r, c]
