@@ -37,7 +37,8 @@ namespace lp {
 // first sub-chunk, sweep one compact region of the matrix.
 // The activations of a sub-chunk are staged once per workgroup into LDS in
 // MFMA-fragment order (one 1 KB block per (k-step, m-tile), lane-major), so
-// they never occupy the vector-memory counter the weight prefetch waits on.
+// they never occupy the vector-memory counter the weight prefetch waits on;
+// each wave loads whole 128-byte row segments of them.
 // The loop body has no exit between a prefetch and its use, and prefetches
 // past the end re-read the last sub-chunk, so the compiler's wait counts stay
 // exact.  Columns of the workgroup's chunk beyond K are zeroed in LDS; the
@@ -71,14 +72,19 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
 #pragma unroll
   for (int j = 0; j < NS; ++j) wrow[j] = W + (int64_t)min((n0 >> 4) + j, nsl - 1) * WT_ELEMS + lane * 8;
   const int64_t wstep = (int64_t)nsl * WT_ELEMS;  // one tile further along K
+  // staging of activation element e (16 bytes): thread e loads row
+  // e / (4 KSUB), so a wave reads whole row segments of the sub-chunk, and
+  // stores the bytes at their fragment position (k-step ks, m-tile i, lane l)
   const T *xsrc[XF];
-  int xk[XF];
+  int xk[XF], xd[XF];
 #pragma unroll
   for (int f = 0; f < XF; ++f) {
     const int e = min(tid + f * NW * 64, XT - 1);
-    const int l = e & 63, i = (e >> 6) % MT, ks = (e >> 6) / MT;
-    xsrc[f] = X + (int64_t)min(i * 16 + (l & 15), M - 1) * ldx;
-    xk[f] = ks * 32 + (l >> 4) * 8;
+    const int row = e / (4 * KSUB), c8 = e % (4 * KSUB);
+    const int ks = c8 >> 2, i = row >> 4, l = (row & 15) + 16 * (c8 & 3);
+    xsrc[f] = X + (int64_t)min(row, M - 1) * ldx;
+    xk[f] = c8 * 8;
+    xd[f] = (ks * MT + i) * 64 + l;
   }
   floatx4_t acc[MT][NS];
 #pragma unroll
@@ -95,7 +101,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const T *__restric
   _Pragma("unroll") for (int f = 0; f < XF; ++f) {                                              \
     const int e = tid + f * NW * 64;                                                            \
     if (XT % (NW * 64) == 0 || e < XT)                                                          \
-      XS[(e >> 6) / MT][(e >> 6) % MT][e & 63] = ((kb) + xk[f] < kend) ? XR[f] : z4;            \
+      (&XS[0][0][0])[xd[f]] = ((kb) + xk[f] < kend) ? XR[f] : z4;                              \
   }
 #define SK_WLOAD(WB, kb)                                                                        \
   _Pragma("unroll") for (int ks = 0; ks < KSUB; ++ks) {                                         \
