@@ -133,13 +133,16 @@ def test_tiny_open_loop_replay():
 TOL = {0: 2e-2, lp.LP_FLAG_BF16_ACTIVATIONS: 8e-2}
 
 
+@pytest.mark.parametrize("kv_heads", [4, 1])
 @pytest.mark.parametrize("source", ["blob", "device"])
 @pytest.mark.parametrize("act", [0, lp.LP_FLAG_BF16_ACTIVATIONS])
-def test_tiny_bf16_teacher_forced_logits(act, source):
+def test_tiny_bf16_teacher_forced_logits(act, source, kv_heads):
     """ffn_dim 688 is not a multiple of 32: the down projection's weight tiles
     carry zero padding, written by the host tiling (blob) or left by the
-    engine's clearing of the weight region (device generator)."""
-    shape = synth.ModelShape("tiny-bf16", 2, 256, 4, 4, 688, 1024)
+    engine's clearing of the weight region (device generator).  With one KV
+    head, k and v are 64-row pieces of the fused QKV matrix beside a 256-row
+    q, placed by the host's strided copy or generated in place."""
+    shape = synth.ModelShape("tiny-bf16", 2, 256, 4, kv_heads, 688, 1024)
     w = synth.model_weights(shape, 11)
     rng = np.random.default_rng(2)
     reqs = [synth.Request(i, rng.integers(0, 1024, size=n).astype(np.int32), 6) for i, n in enumerate([32, 1, 70])]
