@@ -58,7 +58,7 @@ extern "C" {
 
 /* Decoder shape.  Llama-style pre-norm decoder: RMSNorm, rotary embeddings
  * (rotate-half pairing), grouped-query attention, SwiGLU MLP, untied LM head,
- * no biases.  head_dim = d_model / n_heads. */
+ * no biases.  head_dim = d_model / n_heads; vocab even and at most 2^21. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, ffn_dim, vocab;
   float rope_theta; /* RoPE base, e.g. 10000                                  */

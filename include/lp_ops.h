@@ -114,7 +114,7 @@ typedef struct {
  * equal candidates weigh at least ceil(Z * floor(top_p * 2^24) / 2^24) (Z the
  * candidates' total); the draw r = floor(Z_kept * u24 / 2^24), u24 the first
  * Philox output word >> 8, picks the kept candidate, in vocabulary order,
- * whose cumulative weight interval holds r. */
+ * whose cumulative weight interval holds r.  V <= 2^21 (LP_EINVAL beyond). */
 int lp_op_sample(const float *logits, int64_t ld, int32_t M, int32_t V, const lp_sample_params *params,
                  int32_t *tokens, void *hip_stream);
 

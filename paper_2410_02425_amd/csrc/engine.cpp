@@ -176,8 +176,8 @@ int check_config(const lp_model_config *c, const lp_engine_options *o, std::stri
   if (hd != 64 && hd != 128) return err = "head_dim must be 64 or 128", LP_EINVAL;
   const int G = c->n_heads / c->n_kv_heads;
   if (G != 1 && G != 2 && G != 4 && G != 8) return err = "query heads per kv head must be 1, 2, 4 or 8", LP_EINVAL;
-  if (c->d_model > 8192 || c->d_model % 8 || c->ffn_dim % 8 || c->vocab % 2)
-    return err = "d_model <= 8192, d_model and ffn_dim multiples of 8, even vocab required", LP_EINVAL;
+  if (c->d_model > 8192 || c->d_model % 8 || c->ffn_dim % 8 || c->vocab % 2 || c->vocab > SAMPLE_MAX_V)
+    return err = "d_model <= 8192, d_model and ffn_dim multiples of 8, even vocab <= 2^21 required", LP_EINVAL;
   if (c->dtype != LP_F32 && c->dtype != LP_BF16) return err = "dtype", LP_EINVAL;
   if (c->dtype == LP_F32 && hd != 64) return err = "the fp32 path supports head_dim 64", LP_EINVAL;
   if (o->max_batch < 1 || o->max_batch > 64) return err = "max_batch must be 1..64", LP_EINVAL;

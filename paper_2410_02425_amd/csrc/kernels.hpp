@@ -147,7 +147,9 @@ struct SampleParams {
 };
 
 // Next token per row under its sampling parameters (see the kernel):
-// tok -> slot_tok[out_slot[m]] (when out_slot) and tok_out[m].
+// tok -> slot_tok[out_slot[m]] (when out_slot) and tok_out[m].  Rows hold at
+// most SAMPLE_MAX_V logits.
+constexpr int SAMPLE_MAX_V = 1 << 21;
 void launch_sample(const float *logits, int64_t ld, int M, int V, const SampleParams *prm, const int32_t *out_slot,
                    int32_t *slot_tok, int32_t *tok_out, hipStream_t s);
 

@@ -160,6 +160,7 @@ extern "C" int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t 
 extern "C" int lp_op_sample(const float *logits, int64_t ld, int32_t M, int32_t V, const lp_sample_params *params,
                             int32_t *tokens, void *stream) {
   OPCHK(logits && params && tokens && M >= 0 && V > 0 && ld >= V, "sample: args");
+  OPCHK(V <= SAMPLE_MAX_V, "sample: rows of at most 2^21 logits");
   static_assert(sizeof(lp_sample_params) == sizeof(SampleParams), "sampling parameter layout");
   launch_sample(logits, ld, M, V, (const SampleParams *)params, nullptr, nullptr, tokens, (hipStream_t)stream);
   return op_status();
