@@ -106,13 +106,20 @@ def test_sample_kernel_matches_oracle(V):
     rng = np.random.default_rng(V)
     rows, logits = [], []
     combos = [(t, k, p) for t in (0.0, 0.5, 1.0, 1.7) for k in (0, 1, 7, 50) for p in (1.0, 0.9, 0.5, 0.05)]
+    # large top-k (more candidates than the kernel keeps in LDS, and first
+    # radix bins larger than its list), top-p near 1, and a flat row
+    combos += [(0.7, 2000, 1.0), (0.7, 2000, 0.9), (1.3, 20000, 1.0), (1.3, 20000, 0.95),
+               (1.0, 0, 0.999), (2.0, 0, 0.9), (1.0, 5000, 0.5), (0.9, 100000, 0.9), (1.0, 300, 0.9)]
     for i, (t, k, p) in enumerate(combos):
+        k = min(k, V)
         scale = (0.3, 2.0, 6.0)[i % 3]
         l = (rng.standard_normal(V) * scale).astype(np.float32)
         if i % 5 == 0:
             l[rng.integers(0, V, 20)] = l.max()          # repeated maxima
         if i % 7 == 0:
             l = np.round(l, 1).astype(np.float32)       # many ties
+        if i == len(combos) - 1:
+            l = np.full(V, 0.25, dtype=np.float32)      # every logit equal
         logits.append(l)
         key = (int(rng.integers(0, 2**32)), int(rng.integers(0, 2**32)))
         ctr = (i, 0, int(rng.integers(0, 1000)))
