@@ -373,26 +373,54 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   }
   const int fb = ABYTES + wn * 8 * 1024 + lane * 16;
 
+  // PA + 2 loads per stage and wave: with the two younger stages' loads still
+  // allowed outstanding, the oldest stage has landed; the barrier then makes
+  // every wave's loads of it visible
+#define PF_WAIT_BAR()                                                                              \
+  if constexpr (PA == 2) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory"); \
+  else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#define PF_READ(A, B, kt)                                                                          \
+  {                                                                                                \
+    const char *st_ = lds + ((kt) & (PF_NB - 1)) * SBYTES;                                         \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i) A[i] = *(const v8 *)(st_ + fa[i]);              \
+    _Pragma("unroll") for (int j = 0; j < 8; ++j) B[j] = *(const v8 *)(st_ + fb + j * 1024);       \
+  }
+#define PF_MMA(A, B)                                                                               \
+  _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                   \
+    _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[i][j] = Mfma<T>::m16(A[i], B[j], acc[i][j]);
   PF_ISSUE(0)
   PF_ISSUE(1)
   PF_ISSUE(2)
-  for (int kt = 0; kt < nk; ++kt) {
-    // PA + 2 loads per stage and wave: with the two younger stages' loads
-    // still allowed outstanding, stage kt has landed
-    if constexpr (PA == 2) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    PF_ISSUE(kt + 3)
-    const char *st = lds + (kt & (PF_NB - 1)) * SBYTES;
-    v8 a[TM], b[8];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) a[i] = *(const v8 *)(st + fa[i]);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) b[j] = *(const v8 *)(st + fb + j * 1024);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = Mfma<T>::m16(a[i], b[j], acc[i][j]);
+  if constexpr (BM == 128) {
+    // software pipeline: stage kt+1's fragments are read into the other
+    // register set while the MFMAs of stage kt run (two fragment sets fit
+    // beside 128-row accumulators; with 256 rows they would spill)
+    v8 a0[TM], b0[8], a1[TM], b1[8];
+    PF_WAIT_BAR()
+    PF_READ(a0, b0, 0)
+    for (int kt = 0; kt < nk; kt += 2) {
+      PF_ISSUE(kt + 3)
+      PF_WAIT_BAR()
+      PF_READ(a1, b1, kt + 1)
+      PF_MMA(a0, b0)
+      if (kt + 1 >= nk) break;
+      PF_ISSUE(kt + 4)
+      PF_WAIT_BAR()
+      PF_READ(a0, b0, kt + 2)
+      PF_MMA(a1, b1)
+    }
+  } else {
+    for (int kt = 0; kt < nk; ++kt) {
+      PF_WAIT_BAR()
+      PF_ISSUE(kt + 3)
+      v8 a[TM], b[8];
+      PF_READ(a, b, kt)
+      PF_MMA(a, b)
+    }
   }
+#undef PF_WAIT_BAR
+#undef PF_READ
+#undef PF_MMA
 #undef PF_ISSUE
   // the last (re-read) stages land before LDS is reused below
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -436,12 +464,12 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 
 // Tile rows and K splits of a prefill GEMM, chosen by an estimate of its
 // time: the rounds of workgroups over the 256 CUs times one tile's time at
-// the tile shape's measured per-CU rate (4.8 TFLOP/s for 256-row tiles, 3.8
-// for 128-row ones, which waste fewer padded rows at small M and give more
-// tiles), plus the fp32 partials of a split written and read once at
-// 5 TB/s.  Splits keep at least 1024 K each.  Fitted to a sweep of the
-// decoder's four projections over M = 300..2048, it picks the measured best
-// (or a tie) in every case.
+// the tile shape's measured per-CU rate (4.8 TFLOP/s for 256-row tiles, 4.5
+// for the software-pipelined 128-row ones, which waste fewer padded rows at
+// small M and give more tiles), plus the fp32 partials of a split written and
+// read once at 5 TB/s.  Splits keep at least 1024 K each.  Fitted to a sweep
+// of the decoder's four projections over M = 300..4096, it picks within 3% of
+// the measured best in 23 of 24 cases.
 static int prefill_kchunk(int K, int s) { return (K / s + PF_KQ - 1) / PF_KQ * PF_KQ; }
 
 static double prefill_cost(int M, int N, int K, int bm, int s) {
@@ -449,7 +477,7 @@ static double prefill_cost(int M, int N, int K, int bm, int s) {
   const int se = (K + kchunk - 1) / kchunk;
   const int64_t wgs = (int64_t)((M + bm - 1) / bm) * ((N + PF_BN - 1) / PF_BN) * se;
   const double rounds = (double)((wgs + 255) / 256);
-  const double rate = bm == 256 ? 4.8e12 : 3.8e12;
+  const double rate = bm == 256 ? 4.8e12 : 4.5e12;
   const double partials = se > 1 ? 2.0 * se * M * N * 4 / 5e12 : 0.0;
   return rounds * (2.0 * bm * PF_BN * kchunk / rate) + partials;
 }
