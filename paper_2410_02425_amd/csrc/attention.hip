@@ -17,7 +17,6 @@ namespace lp {
 typedef unsigned int u32x4_tt __attribute__((ext_vector_type(4)));
 
 constexpr int DEC_CHUNK = 256;  // positions per decode workgroup
-constexpr int MAX_GROUP = 8;    // query heads per kv head
 
 size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx) {
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;

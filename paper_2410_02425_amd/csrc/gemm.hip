@@ -665,8 +665,8 @@ void launch_gemm<f16_t>(const f16_t *X, int64_t ldx, const f16_t *W, int M, int 
 }
 
 template <>
-void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int N, int K, int splits,
-                        float *part, const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
+void launch_gemm<float>(const float *X, int64_t ldx, const float *W, int M, int N, int K, int /*splits*/,
+                        float * /*part*/, const Epi &ep, hipStream_t s, const hipEvent_t *timing) {
   if (M <= 0 || N <= 0) return;
   dim3 grid((N + F_BN - 1) / F_BN, (M + F_BM - 1) / F_BM);
   launch_k(gemm_f32_kernel, grid, 256, s, timing, X, ldx, W, M, N, K, ep);

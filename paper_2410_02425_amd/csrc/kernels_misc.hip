@@ -451,7 +451,7 @@ __global__ __launch_bounds__(SP_T) void sample_kernel(const float *__restrict__ 
             if ((k & pmask) == prefix) atomicAdd((unsigned long long *)&S.hist[(k >> sh) & (nb - 1)], 1ull);
           }
         } else {
-          sp_row(row, V, vec, [&](int c, float l, bool ok) {
+          sp_row(row, V, vec, [&](int, float l, bool ok) {
             const uint32_t k = order_key(l);
             if (ok && (k & pmask) == prefix) atomicAdd((unsigned long long *)&S.hist[(k >> sh) & (nb - 1)], 1ull);
           });
@@ -496,7 +496,7 @@ __global__ __launch_bounds__(SP_T) void sample_kernel(const float *__restrict__ 
         if (topp && q) atomicAdd((unsigned long long *)&S.hist[sp_qbin(q)], (unsigned long long)q);
       }
     } else {
-      sp_row(row, V, vec, [&](int c, float l, bool ok) {
+      sp_row(row, V, vec, [&](int, float l, bool ok) {
         if (ok && order_key(l) >= kmin) {
           const uint64_t q = q_weight(l, mx, inv_t);
           z += q;
@@ -564,7 +564,7 @@ __global__ __launch_bounds__(SP_T) void sample_kernel(const float *__restrict__ 
               atomicAdd((unsigned long long *)&S.hist[(q >> sh) & (nb - 1)], (unsigned long long)q);
           }
         } else {
-          sp_row(row, V, vec, [&](int c, float l, bool ok) {
+          sp_row(row, V, vec, [&](int, float l, bool ok) {
             if (ok && order_key(l) >= kmin) {
               const uint64_t q = q_weight(l, mx, inv_t);
               if ((q & pmask) == prefix && ((q >> sh) & (nb - 1)))
