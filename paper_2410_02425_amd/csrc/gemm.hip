@@ -306,11 +306,11 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 //     chunks of row r are stored XOR-swizzled by (r / 4) % 4, by choosing the
 //     global address each lane loads, so that the 16-row fragment reads are
 //     free of bank conflicts.
-// gridDim.z > 1 splits K: fp32 partials [z][M][N] replace the epilogue.  Rows
-// and columns past M / N read clamped (valid) memory and are never stored;
-// loads past the last stage re-read it into a buffer nobody reads, so every
-// wave's load count (and the wait count) is the same at every stage.  K must
-// be a multiple of 128.
+// More workgroups than output tiles split K: fp32 partials [z][M][N] replace
+// the epilogue.  Rows and columns past M / N read clamped (valid) memory and
+// are never stored; loads past the last stage re-read it into a buffer nobody
+// reads, so every wave's load count (and the wait count) is the same at every
+// stage.  K must be a multiple of 128.
 
 constexpr int PF_BN = 256, PF_BK = 32, PF_NB = 4, PF_NT = 512;
 constexpr int PF_KQ = 128;  // K granularity of a split
@@ -318,7 +318,8 @@ constexpr int PF_KQ = 128;  // K granularity of a split
 template <typename T, int BM>
 __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
-                                                             int kchunk, float *__restrict__ part, Epi ep) {
+                                                             int kchunk, float *__restrict__ part, Epi ep,
+                                                             int xg) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int TM = BM / 64;                            // 16-row MFMA tiles per wave
   constexpr int PA = BM / 128;                           // activation loads per wave and stage
@@ -327,8 +328,33 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   __shared__ __attribute__((aligned(1024))) char lds[PF_NB * SBYTES];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * PF_BN;
-  const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
+  // 1-D grid.  xg == 0: plain order, column tile fastest.  xg > 0 (column
+  // tile count a multiple of 8): XCD-aware order.  Workgroup i runs on XCD
+  // i % 8, and each XCD takes every eighth column tile.  Its i / 8-th
+  // workgroup walks groups of xg row tiles, row tile fastest inside a group
+  // and then the XCD's column tiles.  The rows of a group share the XCD's L2
+  // and stay in the last-level cache while the XCD's weight columns pass.
+  int bx, by, bz;
+  const int gx = (N + PF_BN - 1) / PF_BN, gy = (M + BM - 1) / BM;
+  const bool split = (int)gridDim.x > gx * gy;  // K split over gridDim.x / (gx gy) ranges
+  {
+    const int lin = blockIdx.x;
+    if (xg > 0) {
+      const int cx = gx / 8, t = lin / 8;
+      bz = t / (cx * gy);
+      int r = t % (cx * gy);
+      const int g0 = r / (xg * cx) * xg, ge = min(xg, gy - g0);  // the group's first row tile, its size
+      r -= g0 * cx;
+      by = g0 + r % ge;
+      bx = r / ge * 8 + lin % 8;
+    } else {
+      bx = lin % gx;
+      by = (lin / gx) % gy;
+      bz = lin / (gx * gy);
+    }
+  }
+  const int m0 = by * BM, n0 = bx * PF_BN;
+  const int kb = bz * kchunk, ke = min(K, kb + kchunk);
   const int nk = (ke - kb) / PF_BK;
   const int nsl = (N + WT_ROWS - 1) / WT_ROWS;
   const int64_t wstep = (int64_t)nsl * WT_ELEMS;  // one tile further along K
@@ -427,8 +453,8 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 
   // accumulator (i, j) of lane l: row 4 (l / 16) + r of 16-row tile i, column l % 16 of tile j
   const int wrow = m0 + wm * (BM / 4), wcol = n0 + wn * 128;
-  if (gridDim.z > 1) {
-    float *pz = part + (int64_t)blockIdx.z * M * N;
+  if (split) {
+    float *pz = part + (int64_t)bz * M * N;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -642,11 +668,16 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
     if (splits < 1 || part == nullptr) splits = 1;
     const PrefillPlan p = prefill_plan(M, N, K, splits);
     const int kchunk = prefill_kchunk(K, splits);
-    dim3 grid((N + PF_BN - 1) / PF_BN, (M + p.bm - 1) / p.bm, p.splits);
+    const int gx = (N + PF_BN - 1) / PF_BN;
+    dim3 grid((unsigned)(gx * ((M + p.bm - 1) / p.bm) * p.splits));
+    // XCD-aware order in groups of 16 row tiles for wide weights (measured
+    // 5-9% faster for the 28,672-row gate/up matrix at most M); narrower ones
+    // run fastest in the plain order
+    const int xg = (gx >= 64 && gx % 8 == 0) ? 16 : 0;
     if (p.bm == 256)
-      launch_k(gemm_prefill_kernel<T, 256>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
+      launch_k(gemm_prefill_kernel<T, 256>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     else
-      launch_k(gemm_prefill_kernel<T, 128>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep);
+      launch_k(gemm_prefill_kernel<T, 128>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);

@@ -38,6 +38,9 @@ GEMM_CASES = [
     # pipelined kernel with tails in M and N, split-K, long K
     (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1), (300, 640, 4096, 4),
     (513, 1000, 1024, 2), (777, 6144, 4096, 1), (600, 1536, 14336, 4), (1030, 512, 384, 3),
+    # wide weights (64 column tiles) take the XCD-grouped tile order: a ragged
+    # last group of row tiles and a tail in N, then with split K
+    (4200, 16300, 128, 1), (300, 16300, 1024, 2),
 ]
 
 
