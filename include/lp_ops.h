@@ -4,7 +4,9 @@
  * hipStream_t, NULL for the null stream).  All pointers are device pointers
  * unless stated otherwise; the caller owns every buffer.  Each returns LP_OK or
  * LP_EINVAL (bad sizes; checked before any launch) or LP_EHIP (launch error);
- * lp_last_error(NULL) then holds a message.
+ * lp_last_error(NULL) then holds a message.  A call with no rows (M, rows or
+ * n_seq equal to 0) checks its sizes, then returns LP_OK without a launch or
+ * any memory access; its pointers may be null.
  *
  * `dtype` is LP_F32, LP_BF16 or LP_F16: the element type of weights and
  * activations (bf16 as raw 16-bit patterns).  Accumulation is fp32 in all.

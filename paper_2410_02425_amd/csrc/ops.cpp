@@ -30,9 +30,11 @@ static int op_status() {
 
 extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
                           int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *stream) {
-  OPCHK(X && W && Y && M >= 0 && N > 0 && K > 0, "gemm: bad pointers or sizes");
+  OPCHK(M >= 0 && N > 0 && K > 0, "gemm: bad sizes");
   OPCHK(K % 8 == 0 && N % 2 == 0 && ldx >= K && ldx % 8 == 0, "gemm: K % 8, N % 2, ldx");
   OPCHK(dtype == LP_F32 || dtype == LP_BF16 || dtype == LP_F16, "gemm: dtype");
+  if (M == 0) return LP_OK;  // no rows: nothing is read or written
+  OPCHK(X && W && Y, "gemm: bad pointers");
   hipStream_t s = (hipStream_t)stream;
   Epi ep{};
   ep.kind = EPI_STORE;
@@ -75,7 +77,9 @@ extern "C" int lp_op_pack_weight(int32_t dtype, const void *W, void *W_packed, i
 
 extern "C" int lp_op_rmsnorm(int32_t dtype, float *x, const float *part, int32_t n_part, const float *g, void *y,
                              int32_t rows, int32_t d, float eps, void *stream) {
-  OPCHK(x && g && y && rows >= 0 && d > 0 && d <= 8192 && n_part >= 0 && (n_part == 0 || part), "rmsnorm: args");
+  OPCHK(rows >= 0 && d > 0 && d <= 8192 && n_part >= 0, "rmsnorm: sizes");
+  if (rows == 0) return LP_OK;  // no rows: nothing is read or written
+  OPCHK(x && g && y && (n_part == 0 || part), "rmsnorm: pointers");
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
     launch_rmsnorm<bf16_t>(x, part, n_part, (int64_t)rows * d, nullptr, g, (bf16_t *)y, rows, d, eps, s);
@@ -108,9 +112,10 @@ extern "C" int lp_op_decode_attention(int32_t dtype, const void *q, void *out, c
                                       void *ws, size_t ws_bytes, void *stream) {
   int rc = check_heads(n_heads, n_kv_heads, head_dim, dtype);
   if (rc) return rc;
-  OPCHK(q && out && k_cache && v_cache && block_table && row_slot && row_pos && M >= 0 && max_ctx > 0,
-        "decode attention: args");
+  OPCHK(M >= 0 && max_ctx > 0, "decode attention: sizes");
   OPCHK(max_blocks * 64 >= max_ctx, "decode attention: max_blocks too small for max_ctx");
+  if (M == 0) return LP_OK;  // no rows: nothing is read or written
+  OPCHK(q && out && k_cache && v_cache && block_table && row_slot && row_pos, "decode attention: pointers");
   OPCHK(ws && ws_bytes >= decode_attention_ws_bytes(M, n_heads, head_dim, max_ctx), "decode attention: ws");
   KVCache kv{(void *)k_cache, (void *)v_cache, block_table, max_blocks, n_blocks, n_kv_heads, head_dim};
   RowMeta rows{row_slot, row_pos};
@@ -134,9 +139,10 @@ extern "C" int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, 
                                        int32_t head_dim, void *stream) {
   int rc = check_heads(n_heads, n_kv_heads, head_dim, dtype);
   if (rc) return rc;
-  OPCHK(q && out && k_cache && v_cache && block_table && seq_start && seq_slot && n_seq >= 0 && max_len > 0,
-        "prefill attention: args");
+  OPCHK(n_seq >= 0 && max_len > 0, "prefill attention: sizes");
   OPCHK(max_blocks * 64 >= max_len, "prefill attention: max_blocks too small for max_len");
+  if (n_seq == 0) return LP_OK;  // no sequences: nothing is read or written
+  OPCHK(q && out && k_cache && v_cache && block_table && seq_start && seq_slot, "prefill attention: pointers");
   KVCache kv{(void *)k_cache, (void *)v_cache, block_table, max_blocks, n_blocks, n_kv_heads, head_dim};
   hipStream_t s = (hipStream_t)stream;
   if (dtype == LP_BF16)
@@ -152,15 +158,19 @@ extern "C" int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, 
 }
 
 extern "C" int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t *tokens, void *stream) {
-  OPCHK(logits && tokens && M >= 0 && V > 0 && ld >= V, "argmax: args");
+  OPCHK(M >= 0 && V > 0 && ld >= V, "argmax: sizes");
+  if (M == 0) return LP_OK;  // no rows: nothing is read or written
+  OPCHK(logits && tokens, "argmax: pointers");
   launch_argmax(logits, ld, M, V, nullptr, nullptr, tokens, (hipStream_t)stream);
   return op_status();
 }
 
 extern "C" int lp_op_sample(const float *logits, int64_t ld, int32_t M, int32_t V, const lp_sample_params *params,
                             int32_t *tokens, void *stream) {
-  OPCHK(logits && params && tokens && M >= 0 && V > 0 && ld >= V, "sample: args");
+  OPCHK(M >= 0 && V > 0 && ld >= V, "sample: sizes");
   OPCHK(V <= SAMPLE_MAX_V, "sample: rows of at most 2^21 logits");
+  if (M == 0) return LP_OK;  // no rows: nothing is read or written
+  OPCHK(logits && params && tokens, "sample: pointers");
   static_assert(sizeof(lp_sample_params) == sizeof(SampleParams), "sampling parameter layout");
   launch_sample(logits, ld, M, V, (const SampleParams *)params, nullptr, nullptr, tokens, (hipStream_t)stream);
   return op_status();

@@ -148,3 +148,34 @@ def test_latency_summary_rejects_bad_input():
         lp.summarize_latencies([0], [0], [1], [5])
     with pytest.raises(ValueError):
         lp.summarize_latencies([0, 1], [1, 1], [2, 1], [5, 6])
+
+
+def test_zero_row_op_calls_are_noops():
+    """Op calls with no rows check their sizes and return LP_OK without a
+    launch or a memory access, so null pointers pass (no GPU is touched);
+    bad sizes are still LP_EINVAL."""
+    L = lp.lib()
+    F16, OK, EINVAL = lp.LP_F16, lp.LP_OK, lp.LP_EINVAL
+    assert L.lp_op_gemm(F16, None, 64, None, None, 0, 128, 64, 1, None, 0, None) == OK
+    assert L.lp_op_gemm(F16, None, 64, None, None, 0, 128, 64, 4, None, 0, None) == OK
+    assert L.lp_op_gemm(F16, None, 64, None, None, -1, 128, 64, 1, None, 0, None) == EINVAL
+    assert L.lp_op_gemm(F16, None, 64, None, None, 0, 128, 60, 1, None, 0, None) == EINVAL  # K % 8
+    assert L.lp_op_rmsnorm(F16, None, None, 8, None, None, 0, 4096, 1e-5, None) == OK
+    assert L.lp_op_rmsnorm(F16, None, None, 0, None, None, 0, 9000, 1e-5, None) == EINVAL  # d > 8192
+    assert L.lp_op_decode_attention(F16, None, None, None, None, None, 2, 4, None, None, 0, 32, 8, 128, 128,
+                                    None, 0, None) == OK
+    assert L.lp_op_decode_attention(F16, None, None, None, None, None, 1, 4, None, None, 0, 32, 8, 128, 128,
+                                    None, 0, None) == EINVAL  # max_blocks * 64 < max_ctx
+    assert L.lp_op_decode_attention(F16, None, None, None, None, None, 2, 4, None, None, 0, 32, 3, 128, 128,
+                                    None, 0, None) == EINVAL  # Hq not a multiple of Hkv
+    assert L.lp_op_prefill_attention(F16, None, None, None, None, None, 2, 4, None, None, 0, 100, 32, 8, 128,
+                                     None) == OK
+    assert L.lp_op_prefill_attention(F16, None, None, None, None, None, 2, 4, None, None, -1, 100, 32, 8, 128,
+                                     None) == EINVAL
+    assert L.lp_op_argmax(None, 1000, 0, 1000, None, None) == OK
+    assert L.lp_op_argmax(None, 999, 0, 1000, None, None) == EINVAL  # ld < V
+    assert L.lp_op_sample(None, 1000, 0, 1000, None, None, None) == OK
+    assert L.lp_op_sample(None, 1 << 22, 0, (1 << 21) + 2, None, None, None) == EINVAL  # V > 2^21
+    # rows present but pointers null: rejected before any launch
+    assert L.lp_op_argmax(None, 1000, 3, 1000, None, None) == EINVAL
+    assert L.lp_op_gemm(F16, None, 64, None, None, 5, 128, 64, 1, None, 0, None) == EINVAL

@@ -97,6 +97,36 @@ def test_tiny_fp32_random_gains_mixed_lengths():
     check_accounting(eng, reqs)
 
 
+def test_tiny_degenerate_requests():
+    """Edges of the serving step: a run with nothing submitted is refused
+    (LP_ESTATE), a request longer than max_seq_len is refused at submission
+    (LP_EINVAL); a one-token prompt with one output token and a request whose
+    in_len + out_len is exactly max_seq_len match the oracle bit for bit."""
+    shape = synth.SHAPES["tiny"]
+    w = synth.model_weights(shape, 7)
+    eng = engine_for(shape, 2, 48, max_prefill=64)
+    eng.load_weights(synth.weights_blob(shape, w))
+    with pytest.raises(lp.LPError) as err:
+        eng.run(lp.LP_CLOSED_LOOP, 2)
+    assert err.value.code == lp.LP_ESTATE
+    rng = np.random.default_rng(11)
+    too_long = [synth.Request(0, rng.integers(0, shape.vocab, size=41).astype(np.int32), 8)]
+    with pytest.raises(lp.LPError) as err:
+        eng.submit(too_long)
+    assert err.value.code == lp.LP_EINVAL
+    reqs = [synth.Request(0, rng.integers(0, shape.vocab, size=1).astype(np.int32), 1),
+            synth.Request(1, rng.integers(0, shape.vocab, size=40).astype(np.int32), 8)]
+    eng.submit(reqs)
+    eng.run(lp.LP_CLOSED_LOOP, 2)
+    m = T.Model(cfg_dict(shape), w)
+    for r in reqs:
+        toks, logits = T.generate(m, r.prompt, r.out_len)
+        got = np.stack([eng.logits(r.id, k) for k in range(r.out_len)])
+        assert np.max(np.abs(got - logits)) <= 1e-4
+        np.testing.assert_array_equal(eng.result(r.id)["tokens"], toks)
+    check_accounting(eng, reqs)
+
+
 def test_tiny_open_loop_replay():
     shape = synth.SHAPES["tiny"]
     w = synth.model_weights(shape, 3)

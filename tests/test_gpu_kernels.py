@@ -291,3 +291,22 @@ def test_prefill_attention(dtype, Hq, Hkv, hd, lens):
         tol = attention_tol(dtype, ref, mag)
         assert np.all(np.abs(got[r0:r0 + n] - ref) <= tol), (j, np.max(np.abs(got[r0:r0 + n] - ref)))
         r0 += n
+
+
+def test_zero_row_calls_through_the_binding():
+    """Empty device tensors (null data pointers) through the binding: nothing
+    is launched and the outputs of other calls are untouched."""
+    z16 = torch.empty(0, 256, dtype=torch.float16, device=DEV)
+    Wd = torch.zeros(64, 256, dtype=torch.float16, device=DEV)
+    Y = torch.empty(0, 64, dtype=torch.float32, device=DEV)
+    lp.op_gemm(z16, packed(Wd), Y, 1, None, N=64)
+    x = torch.empty(0, 256, dtype=torch.float32, device=DEV)
+    g = torch.ones(256, dtype=torch.float32, device=DEV)
+    lp.op_rmsnorm(x, g, torch.empty(0, 256, dtype=torch.float16, device=DEV), 1e-5)
+    logits = torch.empty(0, 1000, dtype=torch.float32, device=DEV)
+    tok = torch.full((4,), -7, dtype=torch.int32, device=DEV)
+    lp.op_argmax(logits, tok[:0])
+    prm = torch.empty(0, dtype=torch.uint8, device=DEV)
+    lp.op_sample(logits, prm, tok[:0])
+    torch.cuda.synchronize()
+    assert tok.cpu().tolist() == [-7] * 4
