@@ -507,9 +507,11 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(const T *__restrict__
 // while the current one is used.  S = Q K^T and O += P V are 16x16x32 MFMAs,
 // the softmax is online (running max and sum per row, reduced across the 16
 // lanes of a row by DPP lane moves), and only the diagonal block needs the
-// causal mask.
+// causal mask.  The launch bound (at least two workgroups' worth of waves
+// per SIMD) makes the compiler keep the 128-dim kernel at 148 VGPRs, so three
+// waves share each SIMD and one wave's softmax runs under another's MFMAs.
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void prefill_attn_mfma_kernel(const T *__restrict__ q, T *__restrict__ out,
+__global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__restrict__ q, T *__restrict__ out,
                                                                 const int32_t *seq_start, const int32_t *seq_slot,
                                                                 KVCache kv, int layer, int n_heads) {
   typedef typename Mfma<T>::v8 v8;
