@@ -113,9 +113,10 @@ void launch_rmsnorm(float *x, const float *part, int n_part, int64_t part_stride
 
 // ------------------------------------------------------------------ argmax
 
-// One workgroup of 1024 threads per row, 16-byte loads; each thread keeps the
-// first maximum it meets in increasing index order, and merges prefer the
-// larger value, then the lower index.
+// One workgroup of 1024 threads per row, 16-byte loads, eight of them
+// requested before any is used (a row then costs four memory round trips, not
+// thirty-two).  Merges prefer the larger value, then the lower index: a total
+// order, so the result does not depend on the order of the merges.
 __device__ __forceinline__ void argmax_merge(float &bv, int &bi, float ov, int oi) {
   if (ov > bv || (ov == bv && oi < bi)) {
     bv = ov;
@@ -132,12 +133,21 @@ __global__ __launch_bounds__(1024) void argmax_kernel(const float *__restrict__ 
   float best = -INFINITY;
   int bi = 0x7fffffff;
   const int v4 = ((ld & 3) == 0) ? V >> 2 : 0;
-  for (int c = threadIdx.x; c < v4; c += 1024) {
-    const float4 q = ((const float4 *)row)[c];
-    argmax_merge(best, bi, q.x, 4 * c);
-    argmax_merge(best, bi, q.y, 4 * c + 1);
-    argmax_merge(best, bi, q.z, 4 * c + 2);
-    argmax_merge(best, bi, q.w, 4 * c + 3);
+  constexpr int U = 8;
+  for (int c0 = threadIdx.x; c0 < v4; c0 += 1024 * U) {
+    float4 q[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) q[u] = ((const float4 *)row)[min(c0 + u * 1024, v4 - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * 1024;
+      if (c < v4) {
+        argmax_merge(best, bi, q[u].x, 4 * c);
+        argmax_merge(best, bi, q[u].y, 4 * c + 1);
+        argmax_merge(best, bi, q[u].z, 4 * c + 2);
+        argmax_merge(best, bi, q[u].w, 4 * c + 3);
+      }
+    }
   }
   for (int c = 4 * v4 + threadIdx.x; c < V; c += 1024) argmax_merge(best, bi, row[c], c);
 #pragma unroll

@@ -174,6 +174,22 @@ def test_argmax_ties_and_tail():
     assert out.cpu().numpy()[:4].tolist() == [5, V - 1, 0, 0]
 
 
+@pytest.mark.parametrize("V,ld", [(1001, 1001), (4100, 4104), (33, 36), (8192 * 4 + 3, 8192 * 4 + 4)])
+def test_argmax_strides_and_tails(V, ld):
+    """Row strides that are not a multiple of 4 (scalar path), a partly
+    filled last batch of loads, and a tail past the last 16-byte chunk."""
+    rng = np.random.default_rng(V)
+    full = rng.standard_normal((5, ld)).astype(np.float32)
+    full[0, V - 1] = 9.0                   # the last element of the row
+    full[1, [3, V - 2]] = 7.0              # tie: lowest index
+    full[2, :] = -np.inf                   # all -inf -> 0
+    full[:, V:] = 100.0                    # padding past V is never read
+    out = torch.empty(5, dtype=torch.int32, device=DEV)
+    lp.op_argmax(to_dev(full, torch.float32)[:, :V], out)
+    torch.cuda.synchronize()
+    assert out.cpu().numpy().tolist() == [int(np.argmax(r[:V])) for r in full]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 def test_device_weight_generator_matches_host(dtype):
     rows, cols, tid, seed = 300, 688, 17, 0x1234ABCD5678
