@@ -78,7 +78,6 @@ class Scheduler {
   }
 
   bool finished() const { return done_ == (int)r_.size(); }
-  int n_active() const { return n_active_; }
 
   // Open loop with an empty batch: the time the head request arrives (> now),
   // else -1 (there is something to do now).
