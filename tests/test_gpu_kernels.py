@@ -34,6 +34,9 @@ GEMM_CASES = [
     # M, N, K, splits -- decode kernel (M <= 64) with and without split-K, tails in M, N and K
     (1, 96, 256, 1), (16, 768, 256, 1), (37, 1376, 688, 3), (64, 1024, 256, 2),
     (64, 6144, 4096, 6), (64, 4096, 14336, 8), (5, 2000, 1000, 4),
+    # the 8B-shape decode launches as the engine issues them at 64 rows:
+    # QKV with 5 splits, O with 8
+    (64, 6144, 4096, 5), (64, 4096, 4096, 8),
     # prefill kernels: K not a multiple of 128 (LDS-tiled fallback), then the
     # pipelined kernel with tails in M and N, split-K, long K
     (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1), (300, 640, 4096, 4),
@@ -240,8 +243,13 @@ def attention_tol(dtype, ref, mag):
     return 2 * u * (mag + np.abs(ref)) + 1e-5
 
 
+# a full 8B-shape decode batch: 64 rows, lognormal contexts (median about
+# 600, clipped to 16..4096) as in the closed-loop workload
+FULL_BATCH_CTX = np.clip(np.random.default_rng(8).lognormal(6.4, 0.7, 64), 16, 4096).astype(int).tolist()
+
 DECODE_CASES = [
     # dtype, Hq, Hkv, hd, context lengths
+    ("f16", 32, 8, 128, FULL_BATCH_CTX),
     ("bf16", 32, 8, 128, [1, 63, 64, 65, 256, 257, 700, 5120]),
     ("f16", 32, 8, 128, [1, 63, 64, 65, 256, 257, 700, 5120]),
     ("f16", 64, 8, 128, [129, 4096]),
