@@ -549,7 +549,9 @@ __global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__re
     mrow[i] = -INFINITY;
     lrow[i] = 0.f;
   }
-  const float scale = rsqrtf((float)HD);
+  // scores in base-2 units: e^x = 2^(x log2 e), with the factor folded into
+  // the scale, so each exponential is one v_exp_f32
+  const float scale = rsqrtf((float)HD) * 1.44269504088896341f;
   const int nblk = min(qt + 1, (len + 63) / 64);  // causal: key blocks up to the diagonal
 
   // staging: chunk c of a block -> K: key c / (HD/8), dims (c % (HD/8)) * 8;
@@ -613,11 +615,11 @@ __global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__re
       mx = row16_max(mx);
       // rows past the sequence end see no valid key: keep them finite
       const float mref = (mx == -INFINITY) ? 0.f : mx;
-      const float corr = __expf(mrow[i] - mref);
+      const float corr = __builtin_amdgcn_exp2f(mrow[i] - mref);
       float t = 0.f;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        const float p = __expf(sacc[nt][i] - mref);
+        const float p = __builtin_amdgcn_exp2f(sacc[nt][i] - mref);
         sacc[nt][i] = p;
         t += p;
       }
