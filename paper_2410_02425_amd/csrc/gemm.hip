@@ -195,79 +195,11 @@ __global__ void gemm_finish_kernel(const float *__restrict__ part, int splits, i
   epi_pair<T>(ep, m, n, v0, v1);
 }
 
-// The QKV epilogue's finishing pass.  A pair's row data (slot and position)
-// does not depend on the partials, so it is requested with them, and the
-// rotary factors and the KV block-table entry that depend on it follow while
-// the partials are still in flight: two memory round trips before the
-// stores instead of three.  The arithmetic is the QKV epilogue's.
-template <typename T>
-__global__ void gemm_finish_qkv_kernel(const float *__restrict__ part, int splits, int M, int N, Epi ep) {
-  const int64_t half = (int64_t)N / 2;
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= (int64_t)M * half) return;
-  const int m = (int)(p / half);
-  const int n = (int)(p % half) * 2;
-  const int slot = ep.rows.row_slot[m];
-  const int pos = ep.rows.row_pos[m];
-  constexpr int U = 8;
-  float2 q[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) q[u] = *(const float2 *)(part + ((int64_t)min(u, splits - 1) * M + m) * N + n);
-  const int hd = ep.kv.head_dim;
-  const int qdim = ep.n_heads * hd;
-  const int kvdim = ep.kv.n_kv_heads * hd;
-  const bool is_q = n < qdim, is_v = n >= qdim + kvdim;
-  const int c = is_q ? n : (is_v ? n - qdim - kvdim : n - qdim);
-  const int h = c / hd;
-  const int i = (c % hd) >> 1;  // rotary pair index
-  float cs = 1.f, sn = 0.f;
-  if (!is_v) {
-    cs = ep.rope_cos[(int64_t)pos * (hd >> 1) + i];
-    sn = ep.rope_sin[(int64_t)pos * (hd >> 1) + i];
-  }
-  const int64_t kvb = is_q ? 0 : kv_block_base(ep.kv, ep.layer, slot, pos, h);
-  float v0 = 0.f, v1 = 0.f;
-  for (int s0 = 0; s0 < splits; s0 += U) {
-    if (s0 > 0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        q[u] = *(const float2 *)(part + ((int64_t)min(s0 + u, splits - 1) * M + m) * N + n);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (s0 + u < splits) {
-        v0 += q[u].x;
-        v1 += q[u].y;
-      }
-  }
-  if (is_v) {
-    T *vt = (T *)ep.kv.v + kvb + (pos % KV_BLOCK);
-    vt[(int64_t)(c % hd) * KV_BLOCK] = Act<T>::st(v0);
-    vt[(int64_t)(c % hd + 1) * KV_BLOCK] = Act<T>::st(v1);
-    return;
-  }
-  const float r0 = v0 * cs - v1 * sn;
-  const float r1 = v1 * cs + v0 * sn;
-  if (is_q) {
-    T *qo = (T *)ep.act_out + (int64_t)m * ep.ld_act + h * hd;
-    qo[i] = Act<T>::st(r0);
-    qo[i + (hd >> 1)] = Act<T>::st(r1);
-  } else {
-    T *k = (T *)ep.kv.k + kvb + (int64_t)(pos % KV_BLOCK) * hd;
-    k[i] = Act<T>::st(r0);
-    k[i + (hd >> 1)] = Act<T>::st(r1);
-  }
-}
-
 template <typename T>
 void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &ep, hipStream_t s) {
   const int64_t pairs = (int64_t)M * (N / 2);
   if (pairs <= 0) return;
-  const unsigned grid = (unsigned)((pairs + 255) / 256);
-  if (ep.kind == EPI_QKV)
-    gemm_finish_qkv_kernel<T><<<grid, 256, 0, s>>>(part, splits, M, N, ep);
-  else
-    gemm_finish_kernel<T><<<grid, 256, 0, s>>>(part, splits, M, N, ep);
+  gemm_finish_kernel<T><<<(unsigned)((pairs + 255) / 256), 256, 0, s>>>(part, splits, M, N, ep);
 }
 
 // ------------------------------------------------------------------ big (prefill)
