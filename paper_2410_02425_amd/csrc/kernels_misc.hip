@@ -6,6 +6,10 @@ namespace lp {
 
 // ------------------------------------------------------------------ embedding
 
+// One workgroup per row.  The row is read in 16-byte pieces, four per thread
+// requested before any is stored, so a row of up to 4,096 16-bit (2,048
+// fp32) values costs one memory round trip; rows whose length is not a
+// multiple of the piece take the element loop.
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(const T *__restrict__ E, const int32_t *pool,
                                                     const int32_t *tok_idx, const int32_t *row_slot,
@@ -16,7 +20,29 @@ __global__ __launch_bounds__(256) void embed_kernel(const T *__restrict__ E, con
   const int tok = ti >= 0 ? pool[ti] : slot_tok[row_slot[m]];
   const T *src = E + (int64_t)tok * d;
   float *dst = x + (int64_t)m * d;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Act<T>::ld(src[c]);
+  constexpr int EV = 16 / sizeof(T);  // elements per 16-byte piece
+  constexpr int U = 4;
+  if (d % EV == 0) {
+    const int nv = d / EV;
+    for (int c0 = threadIdx.x; c0 < nv; c0 += 256 * U) {
+      uint4 r[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) r[u] = ((const uint4 *)src)[min(c0 + u * 256, nv - 1)];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * 256;
+        if (c < nv) {
+          const T *e = (const T *)&r[u];
+#pragma unroll
+          for (int k = 0; k < EV; k += 4)
+            *(float4 *)(dst + (int64_t)c * EV + k) =
+                make_float4(Act<T>::ld(e[k]), Act<T>::ld(e[k + 1]), Act<T>::ld(e[k + 2]), Act<T>::ld(e[k + 3]));
+        }
+      }
+    }
+  } else {
+    for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Act<T>::ld(src[c]);
+  }
 }
 
 template <typename T>
