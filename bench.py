@@ -115,67 +115,115 @@ def copy_bandwidth_gbs(torch, reps: int = 10) -> float:
     return 2 * n / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(shape: synth.ModelShape, reqs, seed: int, budget_s: float = 20.0):
-    """The oracle, unchanged, on a bounded sample of the workload: one request
-    (its prompt taken from the workload, length near the mean) generated at
-    depth 1 and 4 with full-width weights, extrapolated linearly in depth to
-    the full model (three layers of difference keep timing noise small).  The
-    number of output tokens is sized from short probes so that the two timed
-    runs take about budget_s.  Returns the oracle's output tokens/s at full
-    depth for that request."""
+def host_info() -> dict:
+    """The host the oracle runs on: CPU model, cores it may use, and the BLAS
+    library numpy calls with its thread count."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = {"vendor": "unknown", "threads": None}
+    try:
+        import threadpoolctl
+        for lib in threadpoolctl.threadpool_info():
+            if lib.get("user_api") == "blas":
+                blas = {"vendor": f"{lib.get('internal_api')} {lib.get('version')}", "threads": lib.get("num_threads")}
+                break
+    except ImportError:
+        pass
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"cpu_model": model, "cores": cores, "cpu_count": os.cpu_count(), "blas": blas["vendor"],
+            "blas_threads": blas["threads"]}
+
+
+def step_contexts(eng, reqs, log, idx):
+    """Context length of every row of decode step idx of the last run: the
+    row's prompt plus the tokens it produced before that step."""
+    end = log[idx]["end_ns"]
+    in_len = {r.id: r.in_len for r in reqs}
+    return [in_len[i] + int(np.sum(eng.token_times(i) < end)) for i in log[idx]["ids"]]
+
+
+def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.0):
+    """The oracle, unchanged (float64, one request at a time, as it is
+    written), on a bounded sample of a full-batch decode step of the
+    benchmark run: ``ctxs`` are the context lengths of that step's rows.  A
+    sample of the rows, spread over their contexts, runs one decode step
+    (oracle.transformer.decode_step_batch) at depth 1 and 2 with full-width
+    weights; the KV caches hold seeded random values of each row's context
+    length (the step's cost does not depend on them).  The per-layer time is
+    the difference, extrapolated linearly to the full depth, and the rows'
+    time scales with their count because the oracle processes them one by
+    one.  The sample size comes from a one-row probe so that the timed runs
+    take about budget_s.  Returns decode tokens/s of the whole step."""
     from oracle import transformer as T
 
-    r = sorted(reqs, key=lambda q: abs(q.in_len - 553))[0]
-    lm_rows = None
-    embed_rows = None
     models = {}
-    for depth in (1, 4):
+    for depth in (1, 2):
         sh = shape.with_layers(depth)
         w = {}
-        used = np.unique(r.prompt)
         for name, tid, (rows, cols) in synth.tensor_shapes(sh):
             if name == "embed":
-                if embed_rows is None:
-                    embed_rows = np.zeros((rows, cols), dtype=np.float32)
-                    embed_rows[used] = synth.tensor_values(seed, tid, used, cols, 0.02, sh.dtype)
-                w[name] = embed_rows
+                w[name] = np.zeros((1, cols), dtype=np.float32)  # token 0's row, the one fed; set below
+                emb_tid, emb_cols = tid, cols
             elif name == "lm_head":
-                if lm_rows is None:
-                    lm_rows = synth.tensor_values(seed, 2 + 9 * shape.n_layers, np.arange(rows), cols, 0.02,
-                                                  sh.dtype)
-                w[name] = lm_rows
+                w[name] = models[1].w["lm_head"] if depth == 2 else synth.tensor_values(
+                    seed, 2 + 9 * shape.n_layers, np.arange(rows), cols, 0.02, sh.dtype)
             else:
                 v = synth.tensor_values(seed, tid, np.arange(rows), cols, 0.02, sh.dtype, gain=synth.is_gain(name))
                 w[name] = v.reshape(cols) if rows == 1 else v
         cfg = dict(n_layers=depth, d_model=sh.d_model, n_heads=sh.n_heads, n_kv_heads=sh.n_kv_heads,
                    ffn_dim=sh.ffn_dim, vocab=sh.vocab, rope_theta=sh.rope_theta, norm_eps=sh.norm_eps)
         models[depth] = T.Model(cfg, w)
-    # probes at depth 4: prefill alone (1 token) and prefill + 3 decode tokens;
-    # size the sample so that both timed runs together take about budget_s
-    t0 = time.perf_counter()
-    T.generate(models[4], r.prompt, 1)
-    t_pre = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    T.generate(models[4], r.prompt, 4)
-    per_tok = max((time.perf_counter() - t0 - t_pre) / 3, 1e-4)
-    n_out = int(min(max(6, (budget_s - 1.4 * t_pre) / (1.4 * per_tok)), 1024))
-    times = {}
-    for depth in (1, 4):
+        models[depth].w["embed"] = synth.tensor_values(seed, emb_tid, [0], emb_cols, 0.02,
+                                                       sh.dtype).astype(np.float64)
+    rng = np.random.default_rng(seed)
+    order = np.argsort(ctxs)
+
+    def caches(m, sample):
+        # a row of context c attends to c positions: c - 1 cached, one appended by the step
+        out = []
+        for c in sample:
+            kv = T.KVCache(m)
+            kv.k = [rng.standard_normal((c - 1, m.Hkv, m.hd)) * 0.5 for _ in range(m.L)]
+            kv.v = [rng.standard_normal((c - 1, m.Hkv, m.hd)) * 0.5 for _ in range(m.L)]
+            out.append(kv)
+        return out
+
+    def timed(depth, sample):
+        cs = caches(models[depth], sample)
         t0 = time.perf_counter()
-        T.generate(models[depth], r.prompt, n_out)
-        times[depth] = time.perf_counter() - t0
-    per_layer = max((times[4] - times[1]) / 3, 1e-9)
-    fixed = max(times[1] - per_layer, 0.0)
-    full = fixed + per_layer * shape.n_layers
-    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+        T.decode_step_batch(models[depth], cs, [0] * len(sample))
+        return time.perf_counter() - t0
+
+    probe = timed(2, [int(np.median(ctxs))])
+    n = int(min(len(ctxs), max(2, budget_s / (1.8 * probe))))
+    sample = [int(ctxs[order[int(i)]]) for i in np.linspace(0, len(ctxs) - 1, n).round()]
+    t1, t2 = timed(1, sample), timed(2, sample)
+    per_layer = max(t2 - t1, 1e-9)
+    fixed = max(t1 - per_layer, 0.0)
+    step_s = (fixed + per_layer * shape.n_layers) * len(ctxs) / n
+    info = host_info()
     return {
-        "value": n_out / full,
-        "unit": "output tokens/s",
-        "cores": cores,
+        "value": round(len(ctxs) / step_s, 3),
+        "unit": "decode tokens/s",
+        "cores": info["blas_threads"] or info["cores"],
         "kind": "oracle",
-        "sample": (f"one 8B-shape request (in_len {r.in_len}, {n_out} output tokens), float64 oracle with "
-                   f"full-width weights at depth 1 ({times[1]:.1f} s) and 4 ({times[4]:.1f} s), extrapolated "
-                   f"linearly to {shape.n_layers} layers"),
+        "precision": "fp64",
+        "cpu_model": info["cpu_model"],
+        "cpu_cores_available": info["cores"],
+        "blas": info["blas"],
+        "blas_threads": info["blas_threads"],
+        "step_s_extrapolated": round(step_s, 3),
+        "sample": (f"one full-batch decode step of the benchmark run ({len(ctxs)} rows, contexts "
+                   f"{min(ctxs)}..{max(ctxs)}, sum {sum(ctxs)}): {n} of its rows spread over the contexts, "
+                   f"float64 oracle with full-width weights at depth 1 ({t1:.1f} s) and 2 ({t2:.1f} s), "
+                   f"extrapolated linearly to {shape.n_layers} layers and to all {len(ctxs)} rows"),
     }
 
 
@@ -314,9 +362,19 @@ def main():
         "prefill_steps": agg["n_prefill_steps"],
         "decode_steps": agg["n_decode_steps"],
         "roofline": roofline,
+        # the same measure for the whole full-batch decode step (every kernel
+        # of the step), the fraction the target is stated for
+        "step_roofline": {"bound": "hbm", "achieved": round(decode_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(decode_gbs / HBM_PEAK_GBS, 4),
+                          "what": f"full-batch decode step ({wl.max_batch} rows)",
+                          "bytes_per_step": int(full_bytes / max(len(full_idx), 1)),
+                          "ms_per_step": round(full_ns / max(len(full_idx), 1) / 1e6, 3),
+                          "steps": len(full_idx)},
     }
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(shape, reqs, key)
+    if not args.no_cpu_baseline and full_idx:
+        # the full-batch decode step whose context sum is the median one
+        med = sorted(full_idx, key=lambda i: log[i]["sum_ctx"])[len(full_idx) // 2]
+        result["cpu_baseline"] = cpu_baseline(shape, step_contexts(eng, reqs, log, med), key)
     eng.close()
     print(json.dumps(result))
 

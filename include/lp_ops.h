@@ -25,7 +25,9 @@ extern "C" {
 
 /* Y[M x N] (fp32, row stride N) = X[M x K] (row stride ldx) times W[N x K]^T:
  * the weight-GEMM contraction of every projection of the decoder (Q/K/V,
- * output, gate/up, down, LM head).  For LP_BF16 / LP_F16, W is in the tiled
+ * output, gate/up, down, LM head) that both phases of Sec. II-A run every
+ * token through (the paper fixes no layer math; the Llama-style decoder is
+ * a reading).  For LP_BF16 / LP_F16, W is in the tiled
  * weight layout that lp_op_pack_weight writes; for LP_F32 it is row-major
  * [N x K].  16-bit types with M <= 64 take the decode kernel, larger M the
  * prefill kernel; `k_splits` > 1 splits K across workgroups (prefill: only
@@ -50,7 +52,9 @@ int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *
 size_t lp_op_packed_weight_bytes(int32_t dtype, int32_t N, int32_t K);
 int lp_op_pack_weight(int32_t dtype, const void *W, void *W_packed, int32_t N, int32_t K, void *hip_stream);
 
-/* RMSNorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g for r < rows; x fp32
+/* RMSNorm of the decoder layer (run by both phases of Sec. II-A; the norm is
+ * a reading of the architecture, which the paper leaves open):
+ * y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g for r < rows; x fp32
  * [rows x d] (first incremented in place by the n_part fp32 partial arrays
  * part[s][rows][d] when n_part > 0), g fp32 [d], y [rows x d] in dtype.
  * d <= 8192. */
@@ -83,8 +87,9 @@ int lp_op_prefill_attention(int32_t dtype, const void *q, void *out, const void 
                             const int32_t *seq_start, const int32_t *seq_slot, int32_t n_seq, int32_t max_len,
                             int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, void *hip_stream);
 
-/* Greedy decoding: tokens[m] = argmax of logits row m (fp32, row stride ld),
- * lowest index on ties. */
+/* Greedy decoding, the token choice of each prefill and decode step of Sec.
+ * II-A under greedy requests: tokens[m] = argmax of logits row m (fp32, row
+ * stride ld), lowest index on ties.  tokens [M] int32 (device). */
 int lp_op_argmax(const float *logits, int64_t ld, int32_t M, int32_t V, int32_t *tokens, void *hip_stream);
 
 /* The device weight generator (see lp_init_weights_random): dst[rows x cols]

@@ -128,6 +128,59 @@ def test_gemm_full_8b_gate_up_sampled(half):
     assert np.all(np.abs(got - ref) <= bound)
 
 
+_LM_CACHE = {}
+
+
+def _lm_head_weight(N, K, half):
+    """One random [N x K] weight per (N, half), kept for the cases that share
+    it: host values, their fp32 copy (exact), and the tiled device matrix."""
+    key = (N, K, half)
+    if key not in _LM_CACHE:
+        _LM_CACHE.clear()
+        g = torch.Generator().manual_seed(N)
+        W = (torch.randn(N, K, generator=g) * 0.02).to(HALF[half])
+        _LM_CACHE[key] = (W, W.float().numpy(), packed(W.to(DEV)))
+    return _LM_CACHE[key]
+
+
+@pytest.mark.parametrize("half", ["bf16", "f16"])
+@pytest.mark.parametrize("N", [128256, 32000])
+@pytest.mark.parametrize("M", [17, 40, 64])
+def test_gemm_lm_head_decode_sampled(M, N, half):
+    """The LM-head launch of a decode step (the last projection of Sec. II-A's
+    decode phase, producing every greedy token) at 17..64 rows: N = 128,256
+    takes the sixteen-wave plan with 2..4 row tiles per wave, N = 32,000 the
+    eight-wave plan.  1,024 sampled outputs, the first and last column and row
+    included, against the float64 product under the fp32-accumulation bound."""
+    K = 4096
+    g = torch.Generator().manual_seed(M * 1000 + N % 997)
+    X = torch.randn(M, K, generator=g).to(HALF[half])
+    W, Wf, Wp = _lm_head_weight(N, K, half)
+    Y = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    lp.op_gemm(X.to(DEV), Wp, Y, 1, None, N=N)
+    torch.cuda.synchronize()
+    Yh = Y.cpu().numpy()
+    assert not np.isnan(Yh).any()                     # every output written
+    rng = np.random.default_rng(M + N)
+    rows, cols = rng.integers(0, M, 1024), rng.integers(0, N, 1024)
+    rows[:4], cols[:4] = [0, M - 1, 0, M - 1], [0, N - 1, N - 1, 0]
+    Xn = X.float().numpy().astype(np.float64)
+    Wc = Wf[cols].astype(np.float64)
+    ref = np.einsum("ik,ik->i", Xn[rows], Wc)
+    bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xn[rows]), np.abs(Wc))
+    assert np.all(np.abs(Yh[rows, cols] - ref) <= bound)
+    # whole last column block and whole last row, where the tails are
+    Wl = Wf[N - 40:].astype(np.float64)
+    ref_c = Xn @ Wl.T
+    bnd_c = 1e-5 * (np.abs(Xn) @ np.abs(Wl).T)
+    assert np.all(np.abs(Yh[:, N - 40:] - ref_c) <= bnd_c)
+    cs = rng.integers(0, N, 4096)
+    Wr = Wf[cs].astype(np.float64)
+    ref_r = Wr @ Xn[M - 1]
+    bnd_r = 1e-5 * (np.abs(Wr) @ np.abs(Xn[M - 1]))
+    assert np.all(np.abs(Yh[M - 1, cs] - ref_r) <= bnd_r)
+
+
 @pytest.mark.parametrize("M,N,K", [(3, 100, 64), (37, 1376, 688), (130, 768, 256)])
 def test_gemm_f32(M, N, K):
     rng = np.random.default_rng(K)

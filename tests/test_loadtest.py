@@ -52,14 +52,21 @@ def test_characterize_tiny_matches_oracle_accounting():
     cfg = lp.make_config(shape)
     eng = lp.Engine(cfg, lp.EngineOptions(4, 64, 0, 4096, 0, 0))
     eng.init_weights_random(3, 0.02)
-    rows = loadtest.characterize(eng, wl, shape.vocab, [1, 2, 4], requests_per_user=2)
-    assert [r["users"] for r in rows] == [1, 2, 4]
+    # 8 and 16 users on 4 slots: the users beyond the running batch queue
+    rows = loadtest.characterize(eng, wl, shape.vocab, [1, 2, 4, 8, 16], requests_per_user=2)
+    assert [r["users"] for r in rows] == [1, 2, 4, 8, 16]
     for r in rows:
         U = r["users"]
         # replay the last run (U users) through the oracle's accounting
         reqs = synth.make_requests(wl, shape.vocab, max(2 * U, 4))
         eng.submit(reqs)
         eng.run(lp.LP_CLOSED_LOOP, U)
+        # the schedule is the oracle's closed-loop policy on the recorded step times
+        log = eng.step_log()
+        sreqs = [S.SimRequest(q.id, q.in_len, q.out_len) for q in reqs]
+        tr = S.simulate(sreqs, 4, eng.max_batch_weight(), 4096, True, U, [st["end_ns"] for st in log])
+        assert [(st.kind, st.ids, st.slots) for st in tr.steps] == [(st["kind"], st["ids"], st["slots"])
+                                                                    for st in log]
         got = eng.latency_summary()
         res = {q.id: eng.result(q.id) for q in reqs}
         toks = {q.id: eng.token_times(q.id).tolist() for q in reqs}
@@ -67,7 +74,9 @@ def test_characterize_tiny_matches_oracle_accounting():
         for k in ("ttft_p50_ns", "nttft_p50_ns", "itl_p50_ns", "e2e_p50_ns", "itl_p90_ns", "output_tokens",
                   "throughput_tok_s"):
             assert got[k] == exp[k], (U, k)
-        assert max(st["n_rows"] for st in eng.step_log()) <= U
+        assert max(st["n_rows"] for st in log) <= min(U, 4)
+        if U > 4:  # more users than slots: the running batch is full
+            assert max(st["n_rows"] for st in log if st["kind"] == "decode") == 4
         assert r["output_tokens"] == sum(q.out_len for q in reqs)
     eng.close()
 
