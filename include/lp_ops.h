@@ -77,6 +77,25 @@ int lp_op_decode_attention(int32_t dtype, const void *q, void *out, const void *
                            int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, void *ws, size_t ws_bytes,
                            void *hip_stream);
 
+/* lp_op_decode_attention without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Arguments, layouts and results
+ * are those of lp_op_decode_attention; the chunk partials go to a static
+ * device array of LP_NOALLOC_SCRATCH_BYTES (32 MiB) that the library holds on
+ * every GPU it runs on until the process ends.  The call allocates and frees
+ * nothing.  LP_EINVAL when lp_op_decode_attention_ws_bytes(M, n_heads,
+ * head_dim, max_ctx) exceeds the array (64 rows of 32 heads of head_dim 128
+ * fit contexts up to 7,936 positions), checked before any device call.  Every
+ * call on one GPU shares that GPU's array: calls that overlap in time on one
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller. */
+#define LP_NOALLOC_SCRATCH_BYTES (32u << 20)
+int lp_op_decode_attention_noalloc(int32_t dtype, const void *q, void *out, const void *k_cache,
+                                   const void *v_cache, const int32_t *block_table, int32_t max_blocks,
+                                   int64_t n_blocks, const int32_t *row_slot, const int32_t *row_pos, int32_t M,
+                                   int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx,
+                                   void *hip_stream);
+
 /* Causal prefill attention of one layer over packed prompts (Sec. II-A's
  * prompt processing): sequence j owns rows [seq_start[j], seq_start[j+1]) of
  * q/out ([rows x Hq x hd]) at positions 0.., and its keys/values are already

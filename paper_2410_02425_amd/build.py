@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblp.so")
-SOURCES = ["kernels_misc.hip", "gemm.hip", "attention.hip", "engine.cpp", "ops.cpp", "metrics.cpp", "workload.cpp"]
+SOURCES = ["kernels_misc.hip", "gemm.hip", "attention.hip", "engine.cpp", "ops.cpp", "metrics.cpp", "workload.cpp", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",

@@ -25,6 +25,7 @@ EXPORTED = [
     "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
     "lp_wg_fit", "lp_wg_info", "lp_wg_bins", "lp_wg_sample", "lp_wg_sample_independent", "lp_wg_free",
     "lp_op_gemm", "lp_op_packed_weight_bytes", "lp_op_pack_weight", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
+    "lp_op_decode_attention_noalloc",
     "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight", "lp_op_sample",
 ]
 
@@ -119,6 +120,8 @@ def lib():
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
             "lp_op_decode_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp, sz,
                                        vp],
+            "lp_op_decode_attention_noalloc": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32,
+                                               vp],
             "lp_op_prefill_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp],
             "lp_op_argmax": [vp, i64, i32, i32, vp, vp],
             "lp_op_init_weight": [i32, vp, C.c_uint64, i32, i64, i64, f32, vp],
@@ -449,6 +452,14 @@ def op_decode_attention(q, out, kc, vc, block_table, row_slot, row_pos, n_kv_hea
                                         block_table.shape[1], kc.shape[0], _ptr(row_slot), _ptr(row_pos), M, Hq,
                                         n_kv_heads, hd, max_ctx, _ptr(ws), ws.numel() * ws.element_size(),
                                         _stream()))
+
+
+def op_decode_attention_noalloc(q, out, kc, vc, block_table, row_slot, row_pos, n_kv_heads, max_ctx):
+    """lp_op_decode_attention_noalloc: the same call without a workspace."""
+    M, Hq, hd = q.shape
+    _check(lib().lp_op_decode_attention_noalloc(_dt(q), _ptr(q), _ptr(out), _ptr(kc), _ptr(vc), _ptr(block_table),
+                                                block_table.shape[1], kc.shape[0], _ptr(row_slot), _ptr(row_pos), M,
+                                                Hq, n_kv_heads, hd, max_ctx, _stream()))
 
 
 def op_prefill_attention(q, out, kc, vc, block_table, seq_start, seq_slot, max_len, n_kv_heads):
