@@ -301,10 +301,13 @@ def main():
     full_ns = sum(log[i]["end_ns"] - prev_end[i] for i in full_idx)
     if args.step_log:
         with open(args.step_log, "w") as f:
+            in_len_of = {r.id: r.in_len for r in reqs}
             json.dump([{"kind": st["kind"], "n_rows": st["n_rows"], "sum_ctx": st["sum_ctx"],
                         "ns": st["end_ns"] - prev_end[i],
                         "bytes": decode_step_bytes(shape, st["n_rows"], st["sum_ctx"])
-                        if st["kind"] == "decode" else None} for i, st in enumerate(log)], f)
+                        if st["kind"] == "decode" else None,
+                        "prompt_lens": [in_len_of[j] for j in st["ids"]] if st["kind"] == "prefill" else None}
+                       for i, st in enumerate(log)], f)
     full_bytes = sum(decode_step_bytes(shape, log[i]["n_rows"], log[i]["sum_ctx"]) for i in full_idx)
     full_tokens = sum(log[i]["n_rows"] for i in full_idx)
     decode_gbs = full_bytes / full_ns if full_ns else 0.0
