@@ -37,6 +37,16 @@ extern "C" {
 int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *Y, int32_t M, int32_t N,
                int32_t K, int32_t k_splits, void *ws, size_t ws_bytes, void *hip_stream);
 
+/* Which kernel lp_op_gemm (16-bit types) runs for this shape and split
+ * request, for the same contraction as above: `kind` 0 = decode kernel
+ * (M <= 64), 1 = prefill kernel with one workgroup per CU, 2 = prefill
+ * kernel with two 128-row workgroups per CU, 3 = LDS-tiled kernel (K not a
+ * multiple of 128); `tile_rows` = rows per output tile; `splits` = the K
+ * splits it uses.  Host-only, no device call.  Returns LP_EINVAL for
+ * non-positive sizes or null outputs. */
+int lp_op_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t k_splits, int32_t *kind, int32_t *tile_rows,
+                    int32_t *splits);
+
 /* The tiled weight layout of the 16-bit GEMMs (weights of Sec. II-A's
  * decoder, stored for the decode phase's weight stream).  A row-major [N x K]
  * matrix W (row n = output feature n, stride K, K % 8 == 0) becomes

@@ -294,11 +294,18 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // = BM/64 x 8 MFMA 16x16x32 tiles), 32-wide K stages.  Operands travel from global memory
 // straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
 // the instruction's LDS base + 16 x lane), with no register staging and no LDS
-// store instructions.  Four stage buffers, three stages in flight: at each
+// store instructions.  NB stage buffers, NB - 1 stages in flight: at each
 // stage a wave waits for its own loads of that stage (the in-order vmcnt
-// counter, with the two younger stages still outstanding), then a barrier
-// makes every wave's loads visible, and the buffer freed by the previous
-// stage is refilled before the MFMAs run.
+// counter, with the younger stages still outstanding), then a barrier makes
+// every wave's loads visible, and the buffer freed by the previous stage is
+// refilled before the MFMAs run.
+//   * One workgroup per CU (NB = 4, 128 or 96 KB of LDS): the 128-row tile
+//     reads the next stage's fragments while the MFMAs of the current one
+//     run (two fragment sets).
+//   * Two workgroups per CU (BM = 128, NB = 3, 72 KB of LDS, at most 128
+//     registers a wave): each workgroup's barriers and epilogue then overlap
+//     the other's MFMAs, which measured 4-8% faster once a GEMM has at least
+//     two tiles per CU.
 //   * A weight stage is one tile per 16-row slice, copied verbatim: its lanes
 //     are already the B operand of a 16x16x32 MFMA, and the 16 tiles of a
 //     stage lie side by side in memory.
@@ -312,11 +319,23 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(const T *__restrict__ X, 
 // reads, so every wave's load count (and the wait count) is the same at every
 // stage.  K must be a multiple of 128.
 
-constexpr int PF_BN = 256, PF_BK = 32, PF_NB = 4, PF_NT = 512;
+constexpr int PF_BN = 256, PF_BK = 32, PF_NT = 512;
 constexpr int PF_KQ = 128;  // K granularity of a split
 
-template <typename T, int BM>
-__global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
+// Waits until at most N vector loads of this wave remain, then joins the
+// workgroup barrier (LDS reads drained first).
+template <int N>
+__device__ __forceinline__ void prefill_wait_barrier() {
+  static_assert(N == 3 || N == 6 || N == 8, "stage wait count");
+  if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 6) asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(3) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// NB stage buffers; WPE waves per SIMD the registers are budgeted for (2: one
+// workgroup per CU, 4: two).
+template <typename T, int BM, int NB, int WPE>
+__global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
                                                              int kchunk, float *__restrict__ part, Epi ep,
                                                              int xg) {
@@ -325,7 +344,8 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   constexpr int PA = BM / 128;                           // activation loads per wave and stage
   constexpr int ABYTES = BM * PF_BK * 2;                 // activation bytes per stage
   constexpr int SBYTES = (BM + PF_BN) * PF_BK * 2;       // bytes per stage buffer
-  __shared__ __attribute__((aligned(1024))) char lds[PF_NB * SBYTES];
+  __shared__ __attribute__((aligned(1024))) char lds[NB * SBYTES];
+  static_assert(NB * SBYTES >= 8 * 16 * 128 * 4, "the epilogue stages 8 KB per wave in the stage buffers");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   // 1-D grid.  xg == 0: plain order, column tile fastest.  xg > 0 (column
@@ -382,7 +402,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
 #define PF_ISSUE(kt)                                                                                 \
   {                                                                                                  \
     const int s_ = min((kt), nk - 1);                                                                \
-    const uint32_t b_ = (uint32_t)(((kt) & (PF_NB - 1)) * SBYTES);                                   \
+    const uint32_t b_ = (uint32_t)(((kt) % NB) * SBYTES);                                           \
     _Pragma("unroll") for (int i = 0; i < PA; ++i) dma16(ga[i] + s_ * PF_BK, la[i] + b_);            \
     _Pragma("unroll") for (int i = 0; i < 2; ++i) dma16(gw[i] + s_ * wstep, lw[i] + b_);             \
   }
@@ -399,38 +419,36 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   }
   const int fb = ABYTES + wn * 8 * 1024 + lane * 16;
 
-  // PA + 2 loads per stage and wave: with the two younger stages' loads still
-  // allowed outstanding, the oldest stage has landed; the barrier then makes
-  // every wave's loads of it visible
-#define PF_WAIT_BAR()                                                                              \
-  if constexpr (PA == 2) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory"); \
-  else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  // PA + 2 loads per stage and wave: with the NB - 2 younger stages' loads
+  // still allowed outstanding, the oldest stage has landed; the barrier then
+  // makes every wave's loads of it visible
+#define PF_WAIT_BAR() prefill_wait_barrier<(PA + 2) * (NB - 2)>();
 #define PF_READ(A, B, kt)                                                                          \
   {                                                                                                \
-    const char *st_ = lds + ((kt) & (PF_NB - 1)) * SBYTES;                                         \
+    const char *st_ = lds + ((kt) % NB) * SBYTES;                                                  \
     _Pragma("unroll") for (int i = 0; i < TM; ++i) A[i] = *(const v8 *)(st_ + fa[i]);              \
     _Pragma("unroll") for (int j = 0; j < 8; ++j) B[j] = *(const v8 *)(st_ + fb + j * 1024);       \
   }
 #define PF_MMA(A, B)                                                                               \
   _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                   \
     _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[i][j] = Mfma<T>::m16(A[i], B[j], acc[i][j]);
-  PF_ISSUE(0)
-  PF_ISSUE(1)
-  PF_ISSUE(2)
-  if constexpr (BM == 128) {
+#pragma unroll
+  for (int p = 0; p < NB - 1; ++p) PF_ISSUE(p)
+  if constexpr (BM == 128 && WPE == 2) {
     // software pipeline: stage kt+1's fragments are read into the other
     // register set while the MFMAs of stage kt run (two fragment sets fit
-    // beside 128-row accumulators; with 256 rows they would spill)
+    // beside 128-row accumulators in a one-workgroup-per-CU register budget;
+    // with 256 rows, or two workgroups per CU, they would spill)
     v8 a0[TM], b0[8], a1[TM], b1[8];
     PF_WAIT_BAR()
     PF_READ(a0, b0, 0)
     for (int kt = 0; kt < nk; kt += 2) {
-      PF_ISSUE(kt + 3)
+      PF_ISSUE(kt + NB - 1)
       PF_WAIT_BAR()
       PF_READ(a1, b1, kt + 1)
       PF_MMA(a0, b0)
       if (kt + 1 >= nk) break;
-      PF_ISSUE(kt + 4)
+      PF_ISSUE(kt + NB)
       PF_WAIT_BAR()
       PF_READ(a0, b0, kt + 2)
       PF_MMA(a1, b1)
@@ -438,7 +456,7 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   } else {
     for (int kt = 0; kt < nk; ++kt) {
       PF_WAIT_BAR()
-      PF_ISSUE(kt + 3)
+      PF_ISSUE(kt + NB - 1)
       v8 a[TM], b[8];
       PF_READ(a, b, kt)
       PF_MMA(a, b)
@@ -488,14 +506,21 @@ __global__ __launch_bounds__(PF_NT) void gemm_prefill_kernel(const T *__restrict
   }
 }
 
-// Tile rows and K splits of a prefill GEMM, chosen by an estimate of its
-// time: the rounds of workgroups over the 256 CUs times one tile's time at
-// the tile shape's measured per-CU rate (4.8 TFLOP/s for 256-row tiles, 4.5
-// for the software-pipelined 128-row ones, which waste fewer padded rows at
-// small M and give more tiles), plus the fp32 partials of a split written and
-// read once at 5 TB/s.  Splits keep at least 1024 K each.  Fitted to a sweep
-// of the decoder's four projections over M = 300..4096, it picks within 3% of
-// the measured best in 23 of 24 cases.
+// Tile rows, K splits and workgroups per CU of a prefill GEMM, chosen by an
+// estimate of its time.
+//   * One workgroup per CU: the rounds of workgroups over the 256 CUs times
+//     one tile's time at the tile shape's measured per-CU rate (4.8 TFLOP/s
+//     for 256-row tiles, 4.5 for the software-pipelined 128-row ones, which
+//     waste fewer padded rows at small M and give more tiles), plus the fp32
+//     partials of a split written and read once at 5 TB/s.  Splits keep at
+//     least 1024 K each.  Fitted to a sweep of the decoder's four projections
+//     over M = 300..4096, it picks within 3% of the measured best in 23 of 24
+//     cases.
+//   * Two 128-row workgroups per CU (only with at least 512 tiles and no
+//     split: with fewer, the dispatcher pairs workgroups on some CUs while
+//     others idle): full rounds of 512 tiles at 4.86 TFLOP/s per CU, then a
+//     remainder of at most 256 tiles one per CU at the single-tile rate, or a
+//     larger one as one more paired round.
 static int prefill_kchunk(int K, int s) { return (K / s + PF_KQ - 1) / PF_KQ * PF_KQ; }
 
 static double prefill_cost(int M, int N, int K, int bm, int s) {
@@ -508,15 +533,27 @@ static double prefill_cost(int M, int N, int K, int bm, int s) {
   return rounds * (2.0 * bm * PF_BN * kchunk / rate) + partials;
 }
 
+static constexpr int64_t PF_PAIR_MIN_TILES = 512;
+
+static double prefill_pair_cost(int M, int N, int K) {
+  const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + PF_BN - 1) / PF_BN);
+  if (tiles < PF_PAIR_MIN_TILES) return -1.0;
+  const double flops = 2.0 * 128 * PF_BN * K;
+  const int64_t rest = tiles % 512;
+  const double tail = rest == 0 ? 0.0 : (rest <= 256 ? flops / 4.5e12 : 2.0 * flops / 4.86e12);
+  return (double)(tiles / 512) * 2.0 * flops / 4.86e12 + tail;
+}
+
 struct PrefillPlan {
   int bm, splits;
+  bool pair;  // two 128-row workgroups per CU
 };
 
 // splits > 0: the caller's split request (rounded to whole K chunks as
-// gemm_effective_splits does), only the tile rows are chosen; splits == 0:
+// gemm_effective_splits does), only the tile shape is chosen; splits == 0:
 // both are chosen, from 1, 2 or 4 splits.
 static PrefillPlan prefill_plan(int M, int N, int K, int splits) {
-  PrefillPlan best{256, 1};
+  PrefillPlan best{256, 1, false};
   if (M <= 64 || K % PF_KQ != 0) return best;
   double tbest = -1.0;
   for (int s : {1, 2, 4}) {
@@ -527,9 +564,13 @@ static PrefillPlan prefill_plan(int M, int N, int K, int splits) {
       if (tbest < 0.0 || t < tbest) {
         tbest = t;
         const int kchunk = prefill_kchunk(K, req);
-        best = {bm, (K + kchunk - 1) / kchunk};
+        best = {bm, (K + kchunk - 1) / kchunk, false};
       }
     }
+  }
+  if (splits <= 1) {
+    const double t = prefill_pair_cost(M, N, K);
+    if (t >= 0.0 && t < tbest) best = {128, 1, true};
   }
   return best;
 }
@@ -615,6 +656,23 @@ SkinnyPlan skinny_plan(int N, int K, int want_splits) {
 
 int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K, splits).splits; }
 
+void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *eff_splits) {
+  if (M <= 64) {
+    *kind = GEMM_KIND_DECODE;
+    *rows = 16 * ((M + 15) / 16);
+    *eff_splits = gemm_effective_splits(M, N, K, splits);
+  } else if (K % PF_KQ == 0) {
+    const PrefillPlan p = prefill_plan(M, N, K, splits <= 1 ? 1 : gemm_effective_splits(M, N, K, splits));
+    *kind = p.pair ? GEMM_KIND_PREFILL_PAIR : GEMM_KIND_PREFILL;
+    *rows = p.bm;
+    *eff_splits = p.splits;
+  } else {
+    *kind = GEMM_KIND_TILED;
+    *rows = BG_BM;
+    *eff_splits = 1;
+  }
+}
+
 int gemm_effective_splits(int M, int N, int K, int splits) {
   if (splits <= 1) return 1;
   if (M <= 64) return skinny_effective_splits(N, K, splits);
@@ -670,14 +728,17 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
     const int kchunk = prefill_kchunk(K, splits);
     const int gx = (N + PF_BN - 1) / PF_BN;
     dim3 grid((unsigned)(gx * ((M + p.bm - 1) / p.bm) * p.splits));
-    // XCD-aware order in groups of 16 row tiles for wide weights (measured
-    // 5-9% faster for the 28,672-row gate/up matrix at most M); narrower ones
-    // run fastest in the plain order
-    const int xg = (gx >= 64 && gx % 8 == 0) ? 16 : 0;
-    if (p.bm == 256)
-      launch_k(gemm_prefill_kernel<T, 256>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
+    // XCD-aware order in groups of 16 row tiles for wide weights with
+    // 256-row tiles (measured 5-9% faster for the 28,672-row gate/up matrix
+    // at most M); 128-row tiles and narrower weights run fastest in the
+    // plain order (3-9% for 128-row gate/up tiles at M = 1024..4223)
+    const int xg = (p.bm == 256 && gx >= 64 && gx % 8 == 0) ? 16 : 0;
+    if (p.pair)
+      launch_k(gemm_prefill_kernel<T, 128, 3, 4>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, 0);
+    else if (p.bm == 256)
+      launch_k(gemm_prefill_kernel<T, 256, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     else
-      launch_k(gemm_prefill_kernel<T, 128>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
+      launch_k(gemm_prefill_kernel<T, 128, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);

@@ -59,6 +59,17 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
   return op_status();
 }
 
+extern "C" int lp_op_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t k_splits, int32_t *kind,
+                               int32_t *tile_rows, int32_t *splits) {
+  OPCHK(M > 0 && N > 0 && K > 0 && kind && tile_rows && splits, "gemm plan: bad sizes or pointers");
+  int k = 0, r = 0, sp = 0;
+  gemm_plan_info(M, N, K, k_splits, &k, &r, &sp);
+  *kind = k;
+  *tile_rows = r;
+  *splits = sp;
+  return LP_OK;
+}
+
 extern "C" size_t lp_op_packed_weight_bytes(int32_t dtype, int32_t N, int32_t K) {
   if ((dtype != LP_BF16 && dtype != LP_F16) || N <= 0 || K <= 0) return 0;
   return (size_t)wpack_elems(N, K) * 2;

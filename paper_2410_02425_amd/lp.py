@@ -24,7 +24,7 @@ EXPORTED = [
     "lp_get_token_times", "lp_get_run_stats", "lp_get_step_log", "lp_get_logits", "lp_last_error",
     "lp_engine_destroy", "lp_sched_simulate", "lp_summarize_latencies", "lp_get_latency_summary",
     "lp_wg_fit", "lp_wg_info", "lp_wg_bins", "lp_wg_sample", "lp_wg_sample_independent", "lp_wg_free",
-    "lp_op_gemm", "lp_op_packed_weight_bytes", "lp_op_pack_weight", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
+    "lp_op_gemm", "lp_op_gemm_plan", "lp_op_packed_weight_bytes", "lp_op_pack_weight", "lp_op_rmsnorm", "lp_op_decode_attention_ws_bytes", "lp_op_decode_attention",
     "lp_op_decode_attention_noalloc",
     "lp_op_prefill_attention", "lp_op_argmax", "lp_op_init_weight", "lp_op_sample",
 ]
@@ -116,6 +116,7 @@ def lib():
             "lp_wg_sample_independent": [vp, P(C.c_double), i64, P(C.c_double)],
             "lp_get_latency_summary": [vp, P(LatencySummary)],
             "lp_op_gemm": [i32, vp, i64, vp, vp, i32, i32, i32, i32, vp, sz, vp],
+            "lp_op_gemm_plan": [i32, i32, i32, i32, P(i32), P(i32), P(i32)],
             "lp_op_pack_weight": [i32, vp, vp, i32, i32, vp],
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
             "lp_op_decode_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp, sz,
@@ -435,6 +436,16 @@ def op_gemm(X, W, Y, k_splits=1, ws=None, N=None):
         N = W.shape[0]
     _check(lib().lp_op_gemm(_dt(X), _ptr(X), X.stride(0), _ptr(W), _ptr(Y), M, N, K, k_splits, _ptr(ws),
                             0 if ws is None else ws.numel() * ws.element_size(), _stream()))
+
+
+GEMM_KINDS = {0: "decode", 1: "prefill", 2: "prefill_pair", 3: "tiled"}
+
+
+def op_gemm_plan(M, N, K, k_splits=1):
+    """(kernel kind, rows per tile, K splits) that op_gemm runs for this shape."""
+    kind, rows, splits = C.c_int32(), C.c_int32(), C.c_int32()
+    _check(lib().lp_op_gemm_plan(M, N, K, k_splits, C.byref(kind), C.byref(rows), C.byref(splits)))
+    return GEMM_KINDS[kind.value], rows.value, splits.value
 
 
 def op_rmsnorm(x, g, y, eps, part=None, n_part=0):

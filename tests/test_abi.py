@@ -179,3 +179,28 @@ def test_zero_row_op_calls_are_noops():
     # rows present but pointers null: rejected before any launch
     assert L.lp_op_argmax(None, 1000, 3, 1000, None, None) == EINVAL
     assert L.lp_op_gemm(F16, None, 64, None, None, 5, 128, 64, 1, None, 0, None) == EINVAL
+
+
+def test_gemm_plan_query():
+    """The host-side GEMM plan: decode kernel for M <= 64, the LDS-tiled kernel
+    when K is not a multiple of 128, two 128-row workgroups per CU only with
+    at least 512 tiles and no K split, split requests kept (rounded to whole
+    128-wide K chunks)."""
+    assert lp.op_gemm_plan(1, 4096, 4096) == ("decode", 16, 1)
+    assert lp.op_gemm_plan(64, 4096, 4096, 8) == ("decode", 64, 8)
+    assert lp.op_gemm_plan(65, 1376, 688) == ("tiled", 128, 1)
+    assert lp.op_gemm_plan(777, 6144, 4096)[0] == "prefill"
+    for M, N, K in [(553, 28672, 4096), (4223, 4096, 14336), (100, 131072, 256), (1500, 12000, 256)]:
+        tiles = -(-M // 128) * -(-N // 256)
+        assert tiles >= 512
+        assert lp.op_gemm_plan(M, N, K) == ("prefill_pair", 128, 1)
+        kind, rows, splits = lp.op_gemm_plan(M, N, K, 2)
+        assert kind == "prefill" and splits == 2
+    # fewer than 512 tiles of 128 rows never pair
+    for M in range(65, 2049, 64):
+        for N in (1024, 4096, 6144):
+            kind, rows, splits = lp.op_gemm_plan(M, N, 4096)
+            if -(-M // 128) * -(-N // 256) < 512:
+                assert kind == "prefill", (M, N)
+    with pytest.raises(lp.LPError):
+        lp.op_gemm_plan(0, 4096, 4096)

@@ -41,10 +41,19 @@ GEMM_CASES = [
     # pipelined kernel with tails in M and N, split-K, long K
     (65, 1376, 688, 1), (200, 768, 256, 1), (300, 640, 4096, 1), (300, 640, 4096, 4),
     (513, 1000, 1024, 2), (777, 6144, 4096, 1), (600, 1536, 14336, 4), (1030, 512, 384, 3),
-    # wide weights (64 column tiles) take the XCD-grouped tile order: a ragged
-    # last group of row tiles and a tail in N, then with split K
-    (4200, 16300, 128, 1), (300, 16300, 1024, 2),
+    # wide weights (64 column tiles) with 256-row tiles take the XCD-grouped
+    # tile order: a ragged last group of row tiles and a tail in N, without
+    # and with split K
+    (600, 16300, 1024, 1), (300, 16300, 1024, 2),
+    # at least 512 tiles of 128 rows: two workgroups per CU, tails in M and N,
+    # one row tile shorter than 128 rows
+    (4200, 16300, 128, 1), (1500, 12000, 256, 1), (100, 131072, 256, 1),
 ]
+
+# the kernel each case above is planned to take (the plan is host logic)
+GEMM_CASE_KINDS = {(600, 16300, 1024, 1): ("prefill", 256), (300, 16300, 1024, 2): ("prefill", 256),
+                   (4200, 16300, 128, 1): ("prefill_pair", 128), (1500, 12000, 256, 1): ("prefill_pair", 128),
+                   (100, 131072, 256, 1): ("prefill_pair", 128)}
 
 
 HALF = {"bf16": torch.bfloat16, "f16": torch.float16}
@@ -93,6 +102,8 @@ def test_pack_weight_layout(N, K, half):
 @pytest.mark.parametrize("half", ["bf16", "f16"])
 @pytest.mark.parametrize("M,N,K,splits", GEMM_CASES)
 def test_gemm_16bit(M, N, K, splits, half):
+    if (M, N, K, splits) in GEMM_CASE_KINDS:
+        assert lp.op_gemm_plan(M, N, K, splits)[:2] == GEMM_CASE_KINDS[(M, N, K, splits)]
     rng = np.random.default_rng(M * 7 + N + K)
     X = bf16_values(rng, (M, K))          # bf16 values are exact in fp16 too
     W = bf16_values(rng, (N, K), 0.02)
@@ -123,6 +134,32 @@ def test_gemm_full_8b_gate_up_sampled(half):
     rows[:2], cols[:2] = [0, M - 1], [0, N - 1]
     Xn, Wn = X.float().numpy().astype(np.float64), W.float().numpy().astype(np.float64)
     got = Y.cpu().numpy()[rows, cols]
+    ref = np.einsum("ik,ik->i", Xn[rows], Wn[cols])
+    bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xn[rows]), np.abs(Wn[cols]))
+    assert np.all(np.abs(got - ref) <= bound)
+
+
+@pytest.mark.parametrize("half", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K", [(553, 28672, 4096), (4223, 4096, 14336)])
+def test_gemm_prefill_8b_sampled(M, N, K, half):
+    """8B-shape prefill projections at sizes that take two workgroups per CU
+    (gate/up of a 553-token prompt, down of a 4,223-token step), checked on
+    1024 sampled outputs plus the first and last row and column, computed one
+    by one in fp64."""
+    assert lp.op_gemm_plan(M, N, K, 1)[0] == "prefill_pair"
+    g = torch.Generator().manual_seed(M + N)
+    X = torch.randn(M, K, generator=g).to(HALF[half])
+    W = (torch.randn(N, K, generator=g) * 0.02).to(HALF[half])
+    Y = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    lp.op_gemm(X.to(DEV), packed(W.to(DEV)), Y, 1, None, N=N)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(M)
+    rows, cols = rng.integers(0, M, 1024), rng.integers(0, N, 1024)
+    rows[:4], cols[:4] = [0, M - 1, 0, M - 1], [0, N - 1, N - 1, 0]
+    Xn, Wn = X.float().numpy().astype(np.float64), W.float().numpy().astype(np.float64)
+    Yc = Y.cpu().numpy()
+    assert not np.isnan(Yc).any()
+    got = Yc[rows, cols]
     ref = np.einsum("ik,ik->i", Xn[rows], Wn[cols])
     bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xn[rows]), np.abs(Wn[cols]))
     assert np.all(np.abs(got - ref) <= bound)
