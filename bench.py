@@ -149,7 +149,7 @@ def step_contexts(eng, reqs, log, idx):
     return [in_len[i] + int(np.sum(eng.token_times(i) < end)) for i in log[idx]["ids"]]
 
 
-def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.0):
+def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.0, prompt_lens=None):
     """The oracle, unchanged (float64, one request at a time, as it is
     written), on a bounded sample of a full-batch decode step of the
     benchmark run: ``ctxs`` are the context lengths of that step's rows.  A
@@ -160,7 +160,11 @@ def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.
     the difference, extrapolated linearly to the full depth, and the rows'
     time scales with their count because the oracle processes them one by
     one.  The sample size comes from a one-row probe so that the timed runs
-    take about budget_s.  Returns decode tokens/s of the whole step."""
+    take about budget_s.  Returns decode tokens/s of the whole step.
+    ``prompt_lens`` (a prefill step of the same run): the oracle prefills
+    each of its prompts (oracle.transformer.forward on a fresh cache, one
+    request at a time) at depth 1 and 2, extrapolated the same way; reported
+    as prefill tokens/s beside the decode figure."""
     from oracle import transformer as T
 
     models = {}
@@ -202,12 +206,36 @@ def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.
         return time.perf_counter() - t0
 
     probe = timed(2, [int(np.median(ctxs))])
-    n = int(min(len(ctxs), max(2, budget_s / (1.8 * probe))))
+    n = int(min(len(ctxs), max(2, budget_s / (3.6 * probe))))
     sample = [int(ctxs[order[int(i)]]) for i in np.linspace(0, len(ctxs) - 1, n).round()]
-    t1, t2 = timed(1, sample), timed(2, sample)
+    # each depth timed twice, alternating, the faster kept: the per-layer
+    # time is a difference of two timings and one slow run would swing it
+    t1 = t2 = float("inf")
+    for _ in range(2):
+        t1, t2 = min(t1, timed(1, sample)), min(t2, timed(2, sample))
     per_layer = max(t2 - t1, 1e-9)
     fixed = max(t1 - per_layer, 0.0)
     step_s = (fixed + per_layer * shape.n_layers) * len(ctxs) / n
+    prefill = {}
+    if prompt_lens:
+        def timed_prefill(depth):
+            t0 = time.perf_counter()
+            for n_tok in prompt_lens:
+                T.forward(models[depth], [0] * int(n_tok), T.KVCache(models[depth]))
+            return time.perf_counter() - t0
+        p1 = p2 = float("inf")
+        for _ in range(2):
+            p1, p2 = min(p1, timed_prefill(1)), min(p2, timed_prefill(2))
+        p_layer = max(p2 - p1, 1e-9)
+        p_s = max(p1 - p_layer, 0.0) + p_layer * shape.n_layers
+        prefill = {
+            "prefill_value": round(sum(prompt_lens) / p_s, 3),
+            "prefill_unit": "prompt tokens/s",
+            "prefill_s_extrapolated": round(p_s, 3),
+            "prefill_sample": (f"one prefill step of the benchmark run ({len(prompt_lens)} prompt(s), "
+                               f"{sum(prompt_lens)} tokens), the median-sized one: float64 oracle at depth 1 "
+                               f"({p1:.1f} s) and 2 ({p2:.1f} s), extrapolated linearly to {shape.n_layers} layers"),
+        }
     info = host_info()
     return {
         "value": round(len(ctxs) / step_s, 3),
@@ -222,8 +250,9 @@ def cpu_baseline(shape: synth.ModelShape, ctxs, seed: int, budget_s: float = 20.
         "step_s_extrapolated": round(step_s, 3),
         "sample": (f"one full-batch decode step of the benchmark run ({len(ctxs)} rows, contexts "
                    f"{min(ctxs)}..{max(ctxs)}, sum {sum(ctxs)}): {n} of its rows spread over the contexts, "
-                   f"float64 oracle with full-width weights at depth 1 ({t1:.1f} s) and 2 ({t2:.1f} s), "
+                   f"float64 oracle with full-width weights at depth 1 ({t1:.1f} s) and 2 ({t2:.1f} s, each the faster of two runs), "
                    f"extrapolated linearly to {shape.n_layers} layers and to all {len(ctxs)} rows"),
+        **prefill,
     }
 
 
@@ -382,7 +411,10 @@ def main():
     if not args.no_cpu_baseline and full_idx:
         # the full-batch decode step whose context sum is the median one
         med = sorted(full_idx, key=lambda i: log[i]["sum_ctx"])[len(full_idx) // 2]
-        result["cpu_baseline"] = cpu_baseline(shape, step_contexts(eng, reqs, log, med), key)
+        # the prefill step whose prompt-token count is the median one
+        pf = sorted(pre_idx, key=lambda i: sum(in_len[j] for j in log[i]["ids"]))
+        pf_lens = [in_len[j] for j in log[pf[len(pf) // 2]]["ids"]] if pf else None
+        result["cpu_baseline"] = cpu_baseline(shape, step_contexts(eng, reqs, log, med), key, prompt_lens=pf_lens)
     eng.close()
     print(json.dumps(result))
 
