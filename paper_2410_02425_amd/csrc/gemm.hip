@@ -11,9 +11,10 @@
 //    across workgroups writes fp32 partials that a finishing pass (or the
 //    next RMSNorm) reduces.
 //  * gemm_prefill: 16-bit MFMA for prefill-sized M when K is a multiple of
-//    128: 256x256 tiles, eight waves, operands loaded straight from global
-//    memory into four LDS stage buffers (three stages in flight), weight
-//    tiles used verbatim as MFMA operands, optional split-K.
+//    128: 256- or 128-row tiles of 256 columns, eight waves, operands loaded
+//    straight from global memory into LDS stage buffers, weight tiles used
+//    verbatim as MFMA operands, optional split-K; one workgroup per CU, or
+//    two 128-row workgroups per CU for launches of at least 512 tiles.
 //  * gemm_big: 16-bit MFMA for the remaining prefill shapes, 128x128x64 tiles
 //    staged in LDS.
 //  * gemm_f32: fp32 FMA tiles for the fp32 model path (any M).
