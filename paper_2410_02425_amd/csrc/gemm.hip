@@ -663,7 +663,9 @@ void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *
     *rows = 16 * ((M + 15) / 16);
     *eff_splits = gemm_effective_splits(M, N, K, splits);
   } else if (K % PF_KQ == 0) {
-    const PrefillPlan p = prefill_plan(M, N, K, splits <= 1 ? 1 : gemm_effective_splits(M, N, K, splits));
+    // 0: the engine's own choice (prefill_gemm_splits), otherwise lp_op_gemm's
+    const int s = splits == 0 ? prefill_gemm_splits(M, N, K) : (splits < 1 ? 1 : gemm_effective_splits(M, N, K, splits));
+    const PrefillPlan p = prefill_plan(M, N, K, s);
     *kind = p.pair ? GEMM_KIND_PREFILL_PAIR : GEMM_KIND_PREFILL;
     *rows = p.bm;
     *eff_splits = p.splits;

@@ -442,7 +442,8 @@ GEMM_KINDS = {0: "decode", 1: "prefill", 2: "prefill_pair", 3: "tiled"}
 
 
 def op_gemm_plan(M, N, K, k_splits=1):
-    """(kernel kind, rows per tile, K splits) that op_gemm runs for this shape."""
+    """(kernel kind, rows per tile, K splits) that op_gemm runs for this shape;
+    k_splits=0: what an engine prefill step of M > 64 rows runs."""
     kind, rows, splits = C.c_int32(), C.c_int32(), C.c_int32()
     _check(lib().lp_op_gemm_plan(M, N, K, k_splits, C.byref(kind), C.byref(rows), C.byref(splits)))
     return GEMM_KINDS[kind.value], rows.value, splits.value

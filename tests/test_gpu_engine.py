@@ -313,7 +313,9 @@ def full_width_check(shape, reqs, forced, act, max_batch, max_seq=512, max_prefi
     for r in reqs:
         eng.set_forced_tokens(r.id, forced[r.id])
     eng.run(lp.LP_CLOSED_LOOP, max_batch)
-    decode_rows = max(s["n_rows"] for s in eng.step_log() if s["kind"] == "decode")
+    log = eng.step_log()
+    decode_rows = max(s["n_rows"] for s in log if s["kind"] == "decode")
+    full_width_check.max_prefill_tokens = max(s["n_tokens"] for s in log if s["kind"] == "prefill")
     got_all = {r.id: np.stack([eng.logits(r.id, k) for k in range(r.out_len)]) for r in reqs}
     eng.close()
     # oracle weights: every layer tensor, the embedding rows used (token ids
@@ -364,6 +366,29 @@ def test_8b_two_layers_64_slots_teacher_forced():
         forced[i] = rng.integers(0, shape.vocab, size=n_out - 1).tolist()
     _, rows = full_width_check(shape, reqs, forced, 0, 64, max_seq=64, max_prefill=4096, n_vocab_rows=1024)
     assert rows == 64
+
+
+def test_8b_two_layers_large_prefill_two_workgroups_per_cu():
+    """A 4,251-token packed prefill at the 8B shape (two layers, 64 prompts of
+    60..72 tokens): QKV (RoPE and the KV append), O (the residual add) and
+    gate/up (the SiLU gate) of that step run the prefill kernel with two
+    128-row workgroups per CU, down a two-way K split folded by the next
+    RMSNorm; then decode steps at 64 rows.  Logits within 2e-2 of the oracle
+    on sampled vocabulary rows (Sec. II-A)."""
+    shape = synth.SHAPES["8b"].with_layers(2)
+    rng = np.random.default_rng(4300)
+    reqs, forced = [], {}
+    for i in range(64):
+        n_in, n_out = int(rng.integers(60, 73)), int(rng.integers(2, 4))
+        reqs.append(synth.Request(i, rng.integers(0, shape.vocab, size=n_in).astype(np.int32), n_out))
+        forced[i] = rng.integers(0, shape.vocab, size=n_out - 1).tolist()
+    M = sum(r.in_len for r in reqs)
+    d, F, hd = shape.d_model, shape.ffn_dim, shape.head_dim
+    plans = [lp.op_gemm_plan(M, N, K, 0)
+             for N, K in [((shape.n_heads + 2 * shape.n_kv_heads) * hd, d), (d, shape.n_heads * hd), (2 * F, d), (d, F)]]
+    assert M == 4251 and [p[0] for p in plans[:3]] == ["prefill_pair"] * 3 and plans[3][2] > 1, plans
+    _, rows = full_width_check(shape, reqs, forced, 0, 64, max_seq=80, max_prefill=8192, n_vocab_rows=1024)
+    assert rows == 64 and full_width_check.max_prefill_tokens == M  # all 64 prompts in one prefill step
 
 
 @pytest.mark.parametrize("name,layers,lens,act", FULL_WIDTH_CASES)
