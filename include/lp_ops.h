@@ -42,12 +42,13 @@ int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void *W, float *
  * (M <= 64), 1 = prefill kernel with one workgroup per CU, 2 = prefill
  * kernel with two 128-row workgroups per CU, 3 = LDS-tiled kernel (K not a
  * multiple of 128); `tile_rows` = rows per output tile; `splits` = the K
- * splits it uses.  `k_splits` as for lp_op_gemm, except that 0 asks for the
+ * splits it uses; `xcd_group` = row tiles per group of the prefill kernel's
+ * XCD-aware tile order, 0 for the plain order.  `k_splits` as for lp_op_gemm, except that 0 asks for the
  * split count a prefill step of the engine chooses by itself for M > 64.
  * Host-only, no device call.  Returns LP_EINVAL for non-positive sizes or
  * null outputs. */
 int lp_op_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t k_splits, int32_t *kind, int32_t *tile_rows,
-                    int32_t *splits);
+                    int32_t *splits, int32_t *xcd_group);
 
 /* The tiled weight layout of the 16-bit GEMMs (weights of Sec. II-A's
  * decoder, stored for the decode phase's weight stream).  A row-major [N x K]

@@ -535,6 +535,15 @@ static double prefill_cost(int M, int N, int K, int bm, int s) {
 }
 
 static constexpr int64_t PF_PAIR_MIN_TILES = 512;
+static constexpr int64_t PF_LLC_BYTES = 256ll << 20;  // MI355X last-level (Infinity) cache
+
+// Row tiles per XCD group of the tile order (0: plain order) for a 16-bit
+// [N x K] weight with bm-row tiles; the reasons are at the launch.
+static int prefill_xcd_group(int N, int K, int bm) {
+  const int gx = (N + PF_BN - 1) / PF_BN;
+  const bool wide = gx >= 64 && gx % 8 == 0;
+  return (wide && (bm == 256 || (int64_t)N * K * 2 > PF_LLC_BYTES)) ? 16 : 0;
+}
 
 static double prefill_pair_cost(int M, int N, int K) {
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + PF_BN - 1) / PF_BN);
@@ -657,7 +666,8 @@ SkinnyPlan skinny_plan(int N, int K, int want_splits) {
 
 int skinny_effective_splits(int N, int K, int splits) { return skinny_plan(N, K, splits).splits; }
 
-void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *eff_splits) {
+void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *eff_splits, int *xcd_group) {
+  *xcd_group = 0;
   if (M <= 64) {
     *kind = GEMM_KIND_DECODE;
     *rows = 16 * ((M + 15) / 16);
@@ -669,6 +679,7 @@ void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *
     *kind = p.pair ? GEMM_KIND_PREFILL_PAIR : GEMM_KIND_PREFILL;
     *rows = p.bm;
     *eff_splits = p.splits;
+    *xcd_group = prefill_xcd_group(N, K, p.bm);
   } else {
     *kind = GEMM_KIND_TILED;
     *rows = BG_BM;
@@ -731,13 +742,17 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
     const int kchunk = prefill_kchunk(K, splits);
     const int gx = (N + PF_BN - 1) / PF_BN;
     dim3 grid((unsigned)(gx * ((M + p.bm - 1) / p.bm) * p.splits));
-    // XCD-aware order in groups of 16 row tiles for wide weights with
-    // 256-row tiles (measured 5-9% faster for the 28,672-row gate/up matrix
-    // at most M); 128-row tiles and narrower weights run fastest in the
-    // plain order (3-9% for 128-row gate/up tiles at M = 1024..4223)
-    const int xg = (p.bm == 256 && gx >= 64 && gx % 8 == 0) ? 16 : 0;
+    // XCD-aware order in groups of 16 row tiles for wide weights (64 or more
+    // column tiles).  256-row tiles always take it (measured 5-9% faster for
+    // the 28,672 x 4,096 gate/up matrix at most M).  128-row tiles take it
+    // only when the weight is larger than the 256 MB last-level cache: in
+    // the plain order each round of row tiles then re-reads it from HBM
+    // (70B gate/up, 57,344 x 8,192: 31-35% slower plain), while a weight
+    // that fits runs 3-9% faster plain (8B gate/up at M = 1,024..4,223).
+    // Narrower weights keep the plain order.
+    const int xg = prefill_xcd_group(N, K, p.bm);
     if (p.pair)
-      launch_k(gemm_prefill_kernel<T, 128, 3, 4>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, 0);
+      launch_k(gemm_prefill_kernel<T, 128, 3, 4>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     else if (p.bm == 256)
       launch_k(gemm_prefill_kernel<T, 256, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
     else

@@ -101,9 +101,10 @@ void launch_gemm(const T *X, int64_t ldx, const T *W, int M, int N, int K, int s
 
 int gemm_effective_splits(int M, int N, int K, int splits);
 // The kernel a launch_gemm of this shape and split request runs: its kind,
-// rows per output tile and effective K splits.
+// rows per output tile, effective K splits and the row tiles per XCD group of
+// its tile order (0: plain order).
 enum GemmKind : int { GEMM_KIND_DECODE = 0, GEMM_KIND_PREFILL = 1, GEMM_KIND_PREFILL_PAIR = 2, GEMM_KIND_TILED = 3 };
-void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *eff_splits);
+void gemm_plan_info(int M, int N, int K, int splits, int *kind, int *rows, int *eff_splits, int *xcd_group);
 // K splits the prefill GEMM (M > 64) takes for its shape (1 when the tile grid
 // fills the chip); an effective count.
 int prefill_gemm_splits(int M, int N, int K);

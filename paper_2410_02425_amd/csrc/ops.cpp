@@ -60,13 +60,14 @@ extern "C" int lp_op_gemm(int32_t dtype, const void *X, int64_t ldx, const void 
 }
 
 extern "C" int lp_op_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t k_splits, int32_t *kind,
-                               int32_t *tile_rows, int32_t *splits) {
-  OPCHK(M > 0 && N > 0 && K > 0 && kind && tile_rows && splits, "gemm plan: bad sizes or pointers");
-  int k = 0, r = 0, sp = 0;
-  gemm_plan_info(M, N, K, k_splits, &k, &r, &sp);
+                               int32_t *tile_rows, int32_t *splits, int32_t *xcd_group) {
+  OPCHK(M > 0 && N > 0 && K > 0 && kind && tile_rows && splits && xcd_group, "gemm plan: bad sizes or pointers");
+  int k = 0, r = 0, sp = 0, xg = 0;
+  gemm_plan_info(M, N, K, k_splits, &k, &r, &sp, &xg);
   *kind = k;
   *tile_rows = r;
   *splits = sp;
+  *xcd_group = xg;
   return LP_OK;
 }
 

@@ -116,7 +116,7 @@ def lib():
             "lp_wg_sample_independent": [vp, P(C.c_double), i64, P(C.c_double)],
             "lp_get_latency_summary": [vp, P(LatencySummary)],
             "lp_op_gemm": [i32, vp, i64, vp, vp, i32, i32, i32, i32, vp, sz, vp],
-            "lp_op_gemm_plan": [i32, i32, i32, i32, P(i32), P(i32), P(i32)],
+            "lp_op_gemm_plan": [i32, i32, i32, i32, P(i32), P(i32), P(i32), P(i32)],
             "lp_op_pack_weight": [i32, vp, vp, i32, i32, vp],
             "lp_op_rmsnorm": [i32, vp, vp, i32, vp, vp, i32, i32, f32, vp],
             "lp_op_decode_attention": [i32, vp, vp, vp, vp, vp, i32, i64, vp, vp, i32, i32, i32, i32, i32, vp, sz,
@@ -441,12 +441,14 @@ def op_gemm(X, W, Y, k_splits=1, ws=None, N=None):
 GEMM_KINDS = {0: "decode", 1: "prefill", 2: "prefill_pair", 3: "tiled"}
 
 
-def op_gemm_plan(M, N, K, k_splits=1):
-    """(kernel kind, rows per tile, K splits) that op_gemm runs for this shape;
-    k_splits=0: what an engine prefill step of M > 64 rows runs."""
-    kind, rows, splits = C.c_int32(), C.c_int32(), C.c_int32()
-    _check(lib().lp_op_gemm_plan(M, N, K, k_splits, C.byref(kind), C.byref(rows), C.byref(splits)))
-    return GEMM_KINDS[kind.value], rows.value, splits.value
+def op_gemm_plan(M, N, K, k_splits=1, with_order=False):
+    """(kernel kind, rows per tile, K splits) that op_gemm runs for this shape,
+    plus the row tiles per XCD group of its tile order (0: plain) when
+    with_order; k_splits=0: what an engine prefill step of M > 64 rows runs."""
+    kind, rows, splits, xg = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32()
+    _check(lib().lp_op_gemm_plan(M, N, K, k_splits, C.byref(kind), C.byref(rows), C.byref(splits), C.byref(xg)))
+    out = (GEMM_KINDS[kind.value], rows.value, splits.value)
+    return out + (xg.value,) if with_order else out
 
 
 def op_rmsnorm(x, g, y, eps, part=None, n_part=0):

@@ -202,5 +202,13 @@ def test_gemm_plan_query():
             kind, rows, splits = lp.op_gemm_plan(M, N, 4096)
             if -(-M // 128) * -(-N // 256) < 512:
                 assert kind == "prefill", (M, N)
+    # tile order: XCD groups of 16 row tiles for 64+ column tiles with 256-row
+    # tiles, or with 128-row tiles once the weight exceeds the 256 MB
+    # last-level cache; plain otherwise
+    assert lp.op_gemm_plan(553, 57344, 8192, 0, with_order=True)[3] == 16   # 70B gate/up, 940 MB
+    assert lp.op_gemm_plan(553, 28672, 4096, 0, with_order=True)[3] == 0    # 8B gate/up, 235 MB
+    assert lp.op_gemm_plan(600, 16300, 1024, 1, with_order=True)[3] == 16
+    assert lp.op_gemm_plan(1593, 8192, 28672, 0, with_order=True)[3] == 0   # 32 column tiles
+    assert lp.op_gemm_plan(64, 28672, 4096, 1, with_order=True)[3] == 0     # decode kernel
     with pytest.raises(lp.LPError):
         lp.op_gemm_plan(0, 4096, 4096)

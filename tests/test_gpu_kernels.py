@@ -46,14 +46,16 @@ GEMM_CASES = [
     # and with split K
     (600, 16300, 1024, 1), (300, 16300, 1024, 2),
     # at least 512 tiles of 128 rows: two workgroups per CU, tails in M and N,
-    # one row tile shorter than 128 rows
-    (4200, 16300, 128, 1), (1500, 12000, 256, 1), (100, 131072, 256, 1),
+    # one row tile shorter than 128 rows; a weight larger than the 256 MB
+    # last-level cache takes the XCD-grouped order there too
+    (4200, 16300, 128, 1), (1500, 12000, 256, 1), (100, 131072, 256, 1), (600, 34800, 4096, 1),
 ]
 
-# the kernel each case above is planned to take (the plan is host logic)
-GEMM_CASE_KINDS = {(600, 16300, 1024, 1): ("prefill", 256), (300, 16300, 1024, 2): ("prefill", 256),
-                   (4200, 16300, 128, 1): ("prefill_pair", 128), (1500, 12000, 256, 1): ("prefill_pair", 128),
-                   (100, 131072, 256, 1): ("prefill_pair", 128)}
+# the kernel each case above is planned to take (the plan is host logic):
+# kind, tile rows, row tiles per XCD group of the tile order (0: plain)
+GEMM_CASE_KINDS = {(600, 16300, 1024, 1): ("prefill", 256, 16), (300, 16300, 1024, 2): ("prefill", 256, 16),
+                   (4200, 16300, 128, 1): ("prefill_pair", 128, 0), (1500, 12000, 256, 1): ("prefill_pair", 128, 0),
+                   (100, 131072, 256, 1): ("prefill_pair", 128, 0), (600, 34800, 4096, 1): ("prefill_pair", 128, 16)}
 
 
 HALF = {"bf16": torch.bfloat16, "f16": torch.float16}
@@ -103,7 +105,8 @@ def test_pack_weight_layout(N, K, half):
 @pytest.mark.parametrize("M,N,K,splits", GEMM_CASES)
 def test_gemm_16bit(M, N, K, splits, half):
     if (M, N, K, splits) in GEMM_CASE_KINDS:
-        assert lp.op_gemm_plan(M, N, K, splits)[:2] == GEMM_CASE_KINDS[(M, N, K, splits)]
+        kind, rows, _, order = lp.op_gemm_plan(M, N, K, splits, with_order=True)
+        assert (kind, rows, order) == GEMM_CASE_KINDS[(M, N, K, splits)]
     rng = np.random.default_rng(M * 7 + N + K)
     X = bf16_values(rng, (M, K))          # bf16 values are exact in fp16 too
     W = bf16_values(rng, (N, K), 0.02)
@@ -140,13 +143,15 @@ def test_gemm_full_8b_gate_up_sampled(half):
 
 
 @pytest.mark.parametrize("half", ["bf16", "f16"])
-@pytest.mark.parametrize("M,N,K", [(553, 28672, 4096), (4223, 4096, 14336)])
-def test_gemm_prefill_8b_sampled(M, N, K, half):
-    """8B-shape prefill projections at sizes that take two workgroups per CU
-    (gate/up of a 553-token prompt, down of a 4,223-token step), checked on
-    1024 sampled outputs plus the first and last row and column, computed one
-    by one in fp64."""
-    assert lp.op_gemm_plan(M, N, K, 1)[0] == "prefill_pair"
+@pytest.mark.parametrize("M,N,K,order", [(553, 28672, 4096, 0), (4223, 4096, 14336, 0), (553, 57344, 8192, 16)])
+def test_gemm_prefill_sampled(M, N, K, order, half):
+    """Prefill projections at sizes that take two workgroups per CU (8B
+    gate/up of a 553-token prompt and down of a 4,223-token step, both in the
+    plain tile order; 70B gate/up of a 553-token prompt, whose 940 MB weight
+    takes the XCD-grouped order), checked on 1024 sampled outputs plus the
+    first and last row and column, computed one by one in fp64."""
+    kind, _, _, xg = lp.op_gemm_plan(M, N, K, 1, with_order=True)
+    assert kind == "prefill_pair" and xg == order
     g = torch.Generator().manual_seed(M + N)
     X = torch.randn(M, K, generator=g).to(HALF[half])
     W = (torch.randn(N, K, generator=g) * 0.02).to(HALF[half])
@@ -156,12 +161,13 @@ def test_gemm_prefill_8b_sampled(M, N, K, half):
     rng = np.random.default_rng(M)
     rows, cols = rng.integers(0, M, 1024), rng.integers(0, N, 1024)
     rows[:4], cols[:4] = [0, M - 1, 0, M - 1], [0, N - 1, N - 1, 0]
-    Xn, Wn = X.float().numpy().astype(np.float64), W.float().numpy().astype(np.float64)
+    Xs = X[torch.from_numpy(rows)].float().numpy().astype(np.float64)   # only the sampled rows in fp64
+    Ws = W[torch.from_numpy(cols)].float().numpy().astype(np.float64)
     Yc = Y.cpu().numpy()
     assert not np.isnan(Yc).any()
     got = Yc[rows, cols]
-    ref = np.einsum("ik,ik->i", Xn[rows], Wn[cols])
-    bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xn[rows]), np.abs(Wn[cols]))
+    ref = np.einsum("ik,ik->i", Xs, Ws)
+    bound = 1e-5 * np.einsum("ik,ik->i", np.abs(Xs), np.abs(Ws))
     assert np.all(np.abs(got - ref) <= bound)
 
 
