@@ -339,7 +339,7 @@ template <typename T, int BM, int NB, int WPE>
 __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__restrict__ X, int64_t ldx,
                                                              const T *__restrict__ W, int M, int N, int K,
                                                              int kchunk, float *__restrict__ part, Epi ep,
-                                                             int xg) {
+                                                             int xg, int gx) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int TM = BM / 64;                            // 16-row MFMA tiles per wave
   constexpr int PA = BM / 128;                           // activation loads per wave and stage
@@ -349,14 +349,17 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
   static_assert(NB * SBYTES >= 8 * 16 * 128 * 4, "the epilogue stages 8 KB per wave in the stage buffers");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  // 1-D grid.  xg == 0: plain order, column tile fastest.  xg > 0 (column
-  // tile count a multiple of 8): XCD-aware order.  Workgroup i runs on XCD
-  // i % 8, and each XCD takes every eighth column tile.  Its i / 8-th
-  // workgroup walks groups of xg row tiles, row tile fastest inside a group
-  // and then the XCD's column tiles.  The rows of a group share the XCD's L2
-  // and stay in the last-level cache while the XCD's weight columns pass.
+  // 1-D grid over gx column tiles (the weight's, or that count rounded up
+  // to a multiple of 8; workgroups of the padding columns exit at once).
+  // Workgroup i runs on XCD i % 8, so with gx a multiple of 8 every row tile
+  // of a column runs on one XCD and shares its L2.  xg == 0: plain order,
+  // column tile fastest.  xg > 0 (gx a multiple of 8): XCD-aware order; each
+  // XCD takes every eighth column tile, and its i / 8-th workgroup walks
+  // groups of xg row tiles, row tile fastest inside a group and then the
+  // XCD's column tiles.  The rows of a group share the XCD's L2 and stay in
+  // the last-level cache while the XCD's weight columns pass.
   int bx, by, bz;
-  const int gx = (N + PF_BN - 1) / PF_BN, gy = (M + BM - 1) / BM;
+  const int gxw = (N + PF_BN - 1) / PF_BN, gy = (M + BM - 1) / BM;
   const bool split = (int)gridDim.x > gx * gy;  // K split over gridDim.x / (gx gy) ranges
   {
     const int lin = blockIdx.x;
@@ -374,6 +377,7 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
       bz = lin / (gx * gy);
     }
   }
+  if (bx >= gxw) return;  // a padding column: no tile, before any barrier
   const int m0 = by * BM, n0 = bx * PF_BN;
   const int kb = bz * kchunk, ke = min(K, kb + kchunk);
   const int nk = (ke - kb) / PF_BK;
@@ -537,11 +541,15 @@ static double prefill_cost(int M, int N, int K, int bm, int s) {
 static constexpr int64_t PF_PAIR_MIN_TILES = 512;
 static constexpr int64_t PF_LLC_BYTES = 256ll << 20;  // MI355X last-level (Infinity) cache
 
-// Row tiles per XCD group of the tile order (0: plain order) for a 16-bit
-// [N x K] weight with bm-row tiles; the reasons are at the launch.
-static int prefill_xcd_group(int N, int K, int bm) {
+// Column tiles the prefill grid is laid out over, and row tiles per XCD
+// group of its tile order (0: plain order), for a 16-bit [N x K] weight with
+// bm-row tiles; the reasons are at the launch.
+static int prefill_grid_columns(int N) {
   const int gx = (N + PF_BN - 1) / PF_BN;
-  const bool wide = gx >= 64 && gx % 8 == 0;
+  return gx >= 64 ? (gx + 7) / 8 * 8 : gx;
+}
+static int prefill_xcd_group(int N, int K, int bm) {
+  const bool wide = (N + PF_BN - 1) / PF_BN >= 64;
   return (wide && (bm == 256 || (int64_t)N * K * 2 > PF_LLC_BYTES)) ? 16 : 0;
 }
 
@@ -740,23 +748,28 @@ static void launch_gemm_mfma(const T *X, int64_t ldx, const T *W, int M, int N, 
     if (splits < 1 || part == nullptr) splits = 1;
     const PrefillPlan p = prefill_plan(M, N, K, splits);
     const int kchunk = prefill_kchunk(K, splits);
-    const int gx = (N + PF_BN - 1) / PF_BN;
+    const int gx = prefill_grid_columns(N);
     dim3 grid((unsigned)(gx * ((M + p.bm - 1) / p.bm) * p.splits));
-    // XCD-aware order in groups of 16 row tiles for wide weights (64 or more
-    // column tiles).  256-row tiles always take it (measured 5-9% faster for
-    // the 28,672 x 4,096 gate/up matrix at most M).  128-row tiles take it
-    // only when the weight is larger than the 256 MB last-level cache: in
-    // the plain order each round of row tiles then re-reads it from HBM
-    // (70B gate/up, 57,344 x 8,192: 31-35% slower plain), while a weight
-    // that fits runs 3-9% faster plain (8B gate/up at M = 1,024..4,223).
-    // Narrower weights keep the plain order.
+    // Wide weights (64 or more column tiles) lay the grid over a multiple of
+    // 8 column tiles, so that each column's row tiles share one XCD's L2
+    // (7B gate/up, 86 column tiles: 20-25% faster at M = 700..3,500); the
+    // padding leaves at most one column per XCD idle.  Narrower weights
+    // keep their own count (padding 20 to 24 columns left XCDs 20% uneven).
+    // XCD-aware order in groups of 16 row tiles for wide weights: 256-row
+    // tiles always take it (measured 5-9% faster for the 28,672 x 4,096
+    // gate/up matrix at most M).  128-row tiles take it only when the weight
+    // is larger than the 256 MB last-level cache: in the plain order each
+    // round of row tiles then re-reads it from HBM (70B gate/up, 57,344 x
+    // 8,192: 31-35% slower plain; 13B gate/up, 283 MB: 6-11%), while a
+    // weight that fits runs 3-9% faster plain (8B gate/up at M =
+    // 1,024..4,223).
     const int xg = prefill_xcd_group(N, K, p.bm);
     if (p.pair)
-      launch_k(gemm_prefill_kernel<T, 128, 3, 4>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
+      launch_k(gemm_prefill_kernel<T, 128, 3, 4>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg, gx);
     else if (p.bm == 256)
-      launch_k(gemm_prefill_kernel<T, 256, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
+      launch_k(gemm_prefill_kernel<T, 256, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg, gx);
     else
-      launch_k(gemm_prefill_kernel<T, 128, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg);
+      launch_k(gemm_prefill_kernel<T, 128, 4, 2>, grid, PF_NT, s, timing, X, ldx, W, M, N, K, kchunk, part, ep, xg, gx);
     return;
   }
   dim3 grid((N + BG_BN - 1) / BG_BN, (M + BG_BM - 1) / BG_BM);

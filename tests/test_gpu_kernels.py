@@ -49,13 +49,20 @@ GEMM_CASES = [
     # one row tile shorter than 128 rows; a weight larger than the 256 MB
     # last-level cache takes the XCD-grouped order there too
     (4200, 16300, 128, 1), (1500, 12000, 256, 1), (100, 131072, 256, 1), (600, 34800, 4096, 1),
+    # 64 or more column tiles, not a multiple of 8: the grid is laid out over
+    # the next multiple of 8 and its padding workgroups exit (86 tiles,
+    # plain; 108 tiles of a 283 MB weight, grouped; 65 tiles with 256-row
+    # tiles, grouped, and split K, plain)
+    (700, 22000, 4096, 1), (600, 27600, 5120, 1), (600, 16500, 1024, 1), (300, 16500, 2048, 2),
 ]
 
 # the kernel each case above is planned to take (the plan is host logic):
 # kind, tile rows, row tiles per XCD group of the tile order (0: plain)
 GEMM_CASE_KINDS = {(600, 16300, 1024, 1): ("prefill", 256, 16), (300, 16300, 1024, 2): ("prefill", 256, 16),
                    (4200, 16300, 128, 1): ("prefill_pair", 128, 0), (1500, 12000, 256, 1): ("prefill_pair", 128, 0),
-                   (100, 131072, 256, 1): ("prefill_pair", 128, 0), (600, 34800, 4096, 1): ("prefill_pair", 128, 16)}
+                   (100, 131072, 256, 1): ("prefill_pair", 128, 0), (600, 34800, 4096, 1): ("prefill_pair", 128, 16),
+                   (700, 22000, 4096, 1): ("prefill_pair", 128, 0), (600, 27600, 5120, 1): ("prefill_pair", 128, 16),
+                   (600, 16500, 1024, 1): ("prefill", 256, 16), (300, 16500, 2048, 2): ("prefill", 128, 0)}
 
 
 HALF = {"bf16": torch.bfloat16, "f16": torch.float16}
