@@ -142,6 +142,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char *)p;
 }
 
+// Rotary embedding of one pair (x0, x1) = (dimension i, dimension i + hd/2)
+// at angle theta, cs = cos theta, sn = sin theta.  Every kernel that rotates
+// a pair rounds it the same way: the fused multiply-adds are explicit, and
+// the results are held as fp32 (the empty asm), so that a 16-bit store of
+// them is not fused into a mixed-precision FMA that rounds once to 16 bits.
+__device__ __forceinline__ void rope_rotate(float x0, float x1, float cs, float sn, float &r0, float &r1) {
+  r0 = fmaf(x0, cs, -(x1 * sn));
+  r1 = fmaf(x1, cs, x0 * sn);
+  asm("" : "+v"(r0), "+v"(r1));
+}
+
 // Applies the epilogue to output columns (n, n+1) of row m, n even.
 template <typename T>
 __device__ __forceinline__ void epi_pair(const Epi &ep, int m, int n, float v0, float v1) {
@@ -178,8 +189,8 @@ __device__ __forceinline__ void epi_pair(const Epi &ep, int m, int n, float v0, 
         const int i = (c % hd) >> 1;  // rotary pair index
         const float cs = ep.rope_cos[(int64_t)pos * (hd >> 1) + i];
         const float sn = ep.rope_sin[(int64_t)pos * (hd >> 1) + i];
-        const float r0 = v0 * cs - v1 * sn;
-        const float r1 = v1 * cs + v0 * sn;
+        float r0, r1;
+        rope_rotate(v0, v1, cs, sn, r0, r1);
         if (is_q) {
           T *q = (T *)ep.act_out + (int64_t)m * ep.ld_act + h * hd;
           q[i] = Act<T>::st(r0);

@@ -333,6 +333,109 @@ __device__ __forceinline__ void prefill_wait_barrier() {
   else asm volatile("s_waitcnt vmcnt(3) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Rows of a prefill epilogue pass whose global loads are requested together
+// (a register budget of 128 VGPRs, two workgroups per CU, allows 8).
+constexpr int PF_EPI_ROWS = 8;
+
+// One 16-row MFMA tile row of a prefill wave's accumulators (16 x 128 fp32)
+// into the wave's staging area, row-major with a row stride of PF_STG floats:
+// the 4-float pad puts the 16 rows of one column in distinct LDS banks, for
+// the column-wise reads of the V epilogue.
+constexpr int PF_STG = 132;
+__device__ __forceinline__ void prefill_stage16(const floatx4_t (&acc)[8], float *stg, int lane) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) stg[((lane >> 4) * 4 + r) * PF_STG + j * 16 + (lane & 15)] = acc[j][r];
+}
+
+// QKV epilogue of a prefill tile for one wave: rows wrow .. wrow + 16 TM - 1,
+// this lane's column pair (n, n + 1).  Lane l < 16 TM looks up the KV slot,
+// position and cache block of row wrow + l once, and every row reads them
+// back with readlane; the rotary factors of PF_EPI_ROWS rows are requested
+// before the first of their stores.  Same arithmetic and results as epi_pair.
+template <typename T, int TM>
+__device__ __forceinline__ void prefill_epi_qkv(const Epi &ep, const floatx4_t (&acc)[TM][8], float *stg, int wrow,
+                                                int n, int M, int N, int lane) {
+  const int hd = ep.kv.head_dim, half = hd >> 1;
+  const int qdim = ep.n_heads * hd, kvdim = ep.kv.n_kv_heads * hd;
+  int pos_l = 0, blk_l = 0;
+  if (lane < 16 * TM && wrow + lane < M) {
+    const int m = wrow + lane;
+    const int slot = ep.rows.row_slot[m];
+    pos_l = ep.rows.row_pos[m];
+    blk_l = ep.kv.block_table[(int64_t)slot * ep.kv.max_blocks + pos_l / KV_BLOCK];
+  }
+  const bool ok = n < N, is_q = n < qdim, is_v = n >= qdim + kvdim;
+  const int c = is_q ? n : (is_v ? n - qdim - kvdim : n - qdim);
+  const int h = c / hd, j = c % hd, i = j >> 1;
+  const int64_t layer_blocks = (int64_t)ep.layer * ep.kv.n_blocks;
+  // A wave whose 128 columns are one whole V head writes the transposed
+  // cache column-wise: lane (d4, r) = (lane / 16, lane % 16) stores row r's
+  // dimensions 4 k + d4, so one store covers 16 consecutive rows (positions)
+  // of four dimensions instead of one row across 128 scattered ones.
+  const int n0 = n - lane * 2;  // the wave's first column
+  if (hd == 128 && n0 >= qdim + kvdim && n0 + 128 <= N) {
+    const int r = lane & 15, d4 = lane >> 4;
+    const int hv = (n0 - qdim - kvdim) / hd;
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+      prefill_stage16(acc[t], stg, lane);
+      const int pos = __shfl(pos_l, t * 16 + r, 64);
+      const int blk = __shfl(blk_l, t * 16 + r, 64);
+      const bool live = wrow + t * 16 + r < M;
+      T *vt = (T *)ep.kv.v + ((layer_blocks + blk) * ep.kv.n_kv_heads + hv) * (int64_t)KV_BLOCK * hd + pos % KV_BLOCK;
+      __syncthreads();
+#pragma unroll 16
+      for (int k = 0; k < 32; ++k) {
+        const float v = stg[r * PF_STG + 4 * k + d4];
+        if (live) vt[(int64_t)(4 * k + d4) * KV_BLOCK] = Act<T>::st(v);
+      }
+      __syncthreads();
+    }
+    return;
+  }
+#pragma unroll
+  for (int t = 0; t < TM; ++t) {
+    prefill_stage16(acc[t], stg, lane);
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < 16; g += PF_EPI_ROWS) {
+      float cs[PF_EPI_ROWS], sn[PF_EPI_ROWS];
+#pragma unroll
+      for (int u = 0; u < PF_EPI_ROWS; ++u) {
+        const int pos = __builtin_amdgcn_readlane(pos_l, t * 16 + g + u);
+        const bool rot = ok && !is_v && wrow + t * 16 + g + u < M;
+        cs[u] = rot ? ep.rope_cos[(int64_t)pos * half + i] : 0.f;
+        sn[u] = rot ? ep.rope_sin[(int64_t)pos * half + i] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < PF_EPI_ROWS; ++u) {
+        const int row = g + u, m = wrow + t * 16 + row;
+        const int pos = __builtin_amdgcn_readlane(pos_l, t * 16 + row);
+        const int blk = __builtin_amdgcn_readlane(blk_l, t * 16 + row);
+        const float2 v = *(const float2 *)(stg + row * PF_STG + lane * 2);
+        if (m < M && ok) {
+          const int64_t cb = ((layer_blocks + blk) * ep.kv.n_kv_heads + h) * (int64_t)KV_BLOCK * hd;
+          if (is_v) {
+            T *vt = (T *)ep.kv.v + cb + pos % KV_BLOCK;
+            vt[(int64_t)j * KV_BLOCK] = Act<T>::st(v.x);
+            vt[(int64_t)(j + 1) * KV_BLOCK] = Act<T>::st(v.y);
+          } else {
+            float r0, r1;
+            rope_rotate(v.x, v.y, cs[u], sn[u], r0, r1);
+            T *dst = is_q ? (T *)ep.act_out + (int64_t)m * ep.ld_act + h * hd
+                          : (T *)ep.kv.k + cb + (int64_t)(pos % KV_BLOCK) * hd;
+            dst[i] = Act<T>::st(r0);
+            dst[i + half] = Act<T>::st(r1);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // NB stage buffers; WPE waves per SIMD the registers are budgeted for (2: one
 // workgroup per CU, 4: two).
 template <typename T, int BM, int NB, int WPE>
@@ -346,7 +449,7 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
   constexpr int ABYTES = BM * PF_BK * 2;                 // activation bytes per stage
   constexpr int SBYTES = (BM + PF_BN) * PF_BK * 2;       // bytes per stage buffer
   __shared__ __attribute__((aligned(1024))) char lds[NB * SBYTES];
-  static_assert(NB * SBYTES >= 8 * 16 * 128 * 4, "the epilogue stages 8 KB per wave in the stage buffers");
+  static_assert(NB * SBYTES >= 8 * 16 * PF_STG * 4, "the epilogue stages 16 rows per wave in the stage buffers");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   // 1-D grid over gx column tiles (the weight's, or that count rounded up
@@ -492,20 +595,46 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
     return;
   }
   // epilogue through LDS: each wave stages 16 rows x 128 columns of fp32 at a
-  // time in its own 8 KB, then its lanes apply the epilogue to column pairs,
-  // one 128-column row per pass of the wave
-  float *stg = (float *)lds + wave * 16 * 128;
+  // time in its own 8.25 KB, then its lanes apply the epilogue to column pairs,
+  // one 128-column row per pass of the wave.  What a pass reads from global
+  // memory (residual rows, rotary factors, row metadata) is requested before
+  // its first store: a load issued behind a store also waits for the store.
+  float *stg = (float *)lds + wave * 16 * PF_STG;
+  const int n = wcol + lane * 2;
+  if (ep.kind == EPI_QKV) {
+    prefill_epi_qkv<T, TM>(ep, acc, stg, wrow, n, M, N, lane);
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) stg[((lane >> 4) * 4 + r) * 128 + j * 16 + (lane & 15)] = acc[i][j][r];
+    prefill_stage16(acc[i], stg, lane);
     __syncthreads();
-    for (int row = 0; row < 16; ++row) {
-      const int m = wrow + i * 16 + row, n = wcol + lane * 2;
-      const float2 v = *(const float2 *)(stg + row * 128 + lane * 2);
-      if (m < M && n < N) epi_pair<T>(ep, m, n, v.x, v.y);
+    if (ep.kind == EPI_RESID) {
+#pragma unroll
+      for (int g = 0; g < 16; g += PF_EPI_ROWS) {
+        float2 r[PF_EPI_ROWS];
+#pragma unroll
+        for (int u = 0; u < PF_EPI_ROWS; ++u) {
+          const int m = wrow + i * 16 + g + u;
+          r[u] = (m < M && n < N) ? *(const float2 *)(ep.out + (int64_t)m * ep.ldo + n) : make_float2(0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < PF_EPI_ROWS; ++u) {
+          const int m = wrow + i * 16 + g + u;
+          const float2 v = *(const float2 *)(stg + (g + u) * PF_STG + lane * 2);
+          if (m < M && n < N) {
+            r[u].x += v.x;
+            r[u].y += v.y;
+            *(float2 *)(ep.out + (int64_t)m * ep.ldo + n) = r[u];
+          }
+        }
+      }
+    } else {
+      for (int row = 0; row < 16; ++row) {
+        const int m = wrow + i * 16 + row;
+        const float2 v = *(const float2 *)(stg + row * PF_STG + lane * 2);
+        if (m < M && n < N) epi_pair<T>(ep, m, n, v.x, v.y);
+      }
     }
     __syncthreads();
   }
