@@ -59,6 +59,11 @@ extern "C" {
  * the 2-layer full-width 8B shape (fp16: 7.4e-3) and is held to 8e-2 in its
  * own tests.  Kept as a comparison mode; the benchmark does not use it. */
 #define LP_FLAG_BF16_ACTIVATIONS 4u
+/* Decode steps finish the split-K QKV projection (partial sums, rotary
+ * embedding, KV append) in a pass of its own instead of inside the decode
+ * attention kernel.  A reference path for tests of the fused one: the
+ * results are the same bit for bit, the step takes one launch per layer more. */
+#define LP_FLAG_SEPARATE_QKV_FINISH 8u
 
 /* Decoder shape.  Llama-style pre-norm decoder: RMSNorm, rotary embeddings
  * (rotate-half pairing), grouped-query attention, SwiGLU MLP, untied LM head,

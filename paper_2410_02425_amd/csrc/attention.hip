@@ -25,6 +25,13 @@ size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx) 
 
 int decode_attention_chunks(int ctx) { return (ctx + DEC_CHUNK - 1) / DEC_CHUNK; }
 
+// The fused QKV finish gives each of the 256 threads one q pair of the group
+// and requests all its partials at once.
+constexpr int DEC_QKV_SPLITS = 6;
+bool decode_attention_fuses_qkv(int group, int head_dim, int splits) {
+  return group * head_dim / 2 <= 256 && splits >= 1 && splits <= DEC_QKV_SPLITS;
+}
+
 // Work item -> (row m, chunk s, slot, context) of a decode workgroup.  Item i
 // is the i-th pair in the row-major list of every row's chunks (a row of
 // context c has ceil(c / DEC_CHUNK)); contexts are clamped to max_ctx.  Each
@@ -32,14 +39,15 @@ int decode_attention_chunks(int ctx) { return (ctx + DEC_CHUNK - 1) / DEC_CHUNK;
 // over the 64 lanes gives the chunks up to that row, and the first lane whose
 // running count exceeds the item is the row.  False past the last item.
 struct DecodeItem {
-  int m, s, slot, ctx;
+  int m, s, slot, ctx, pos;
 };
 __device__ __forceinline__ bool decode_item(const RowMeta &rows, int M, int max_ctx, int item, DecodeItem &it) {
   const int lane = threadIdx.x & 63;
   int before = 0;
   for (int base = 0; base < M; base += 64) {
     const int r = base + lane;
-    const int ctx = r < M ? min(rows.row_pos[r] + 1, max_ctx) : 0;
+    const int pos = r < M ? rows.row_pos[r] : 0;
+    const int ctx = r < M ? min(pos + 1, max_ctx) : 0;
     const int slot = r < M ? rows.row_slot[r] : 0;
     const int n = ctx > 0 ? (ctx + DEC_CHUNK - 1) / DEC_CHUNK : 0;
     int incl = n;
@@ -56,6 +64,7 @@ __device__ __forceinline__ bool decode_item(const RowMeta &rows, int M, int max_
       it.s = rel - __shfl(incl - n, k, 64);
       it.slot = __shfl(slot, k, 64);
       it.ctx = __shfl(ctx, k, 64);
+      it.pos = __shfl(pos, k, 64);
       return true;
     }
     before += total;
@@ -255,16 +264,27 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(RowMeta rows, int n_
 // layout, and O = P V contracts over positions with V read from its
 // transposed [hd][64] block as 16-byte B fragments.  All K fragments of the
 // block are requested before any is used, then all V fragments.
-template <typename T, int HD, int G>
-__global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restrict__ q, RowMeta rows, KVCache kv,
-                                                               int layer, int M, int n_heads, int max_ctx,
-                                                               int max_splits, float *__restrict__ ws) {
+//
+// FUSED: q is not read; the workgroup finishes the split-K QKV projection of
+// its row first (QkvParts): the fp32 partials of its G query heads summed in
+// split order and rotated into LDS, and in the workgroup of the row's last
+// chunk the new K (rotated) and V entry of head g, written to the cache and
+// put into the last block's fragments in place of what the cache held there.
+// Its registers are bounded for four waves per SIMD (112 VGPRs, no spills):
+// the 8B-shape decode step ran 75 us faster than with the separate finishing
+// pass, against 41 us at the compiler's own three.
+template <typename T, int HD, int G, bool FUSED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FUSED ? 4 : 1))) void decode_attn_mfma_kernel(
+    const T *__restrict__ q, RowMeta rows, KVCache kv, int layer, int M, int n_heads, int max_ctx, int max_splits,
+    float *__restrict__ ws, QkvParts qp) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int KS = HD / 32;  // contraction steps over head_dim
   constexpr int NT = HD / 16;  // 16-wide output tiles over head_dim
   __shared__ T pls[4][16][64 + 8];
   __shared__ float wm[4][16], wl[4][16];
   __shared__ float wo[4][G][HD];
+  __shared__ T qls[FUSED ? G : 1][HD];   // FUSED: the group's rotated q
+  __shared__ T kvn[FUSED ? 2 : 1][HD];   // FUSED: the row's new K (rotated) and V entry
   // KV head fastest: consecutive block ids, which the dispatcher deals out
   // round-robin over the XCDs, are the heads of one work item
   const int g = blockIdx.x % kv.n_kv_heads;
@@ -276,24 +296,129 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
   const int blk_pos = s * DEC_CHUNK + wave * 64;
   const int nvalid = max(0, min(64, ctx - blk_pos));
 
-  v8 qa[KS];
-  const T *qrow = q + ((int64_t)m * n_heads + g * G + (r16 < G ? r16 : 0)) * HD;
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qa[ks] = (r16 < G) ? load8<T>(qrow + ks * 32 + kq) : zero8<T>();
-
   const int64_t base = nvalid > 0 ? kv_block_base(kv, layer, slot, blk_pos, g) : 0;
   v8 kf[4][KS];
-  if (nvalid > 0) {
-    const T *kb = (const T *)kv.k + base;
+  v8 qa[KS];
+  // the row's new position, when it lies in this wave's block (FUSED)
+  const int pnew = (FUSED && it.pos == ctx - 1) ? it.pos - blk_pos : -1;
+  if constexpr (FUSED) {
+    // Thread t takes q pair t of the group's heads and, in the workgroup of
+    // the row's last chunk, pair t of head g's new K (t < HD/2) or V entry.
+    // All their loads are issued before the K fragments' (the wait counter
+    // is in order), so q is ready when K is.
+    static_assert(G * HD / 2 <= 256, "one q pair per thread (decode_attention_fuses_qkv)");
+    // Every load below is unconditional, at a clamped (valid) address, so
+    // that the compiler issues them back to back and can wait for them
+    // without waiting for the K fragments requested after them.
+    const bool last = (s + 1) * DEC_CHUNK >= ctx && it.pos == ctx - 1;
+    const int pos = it.pos, half = HD / 2, t = threadIdx.x;
+    const int qdim = n_heads * HD, kvdim = kv.n_kv_heads * HD;
+    const bool has_q = t < G * half, has_kv = last && t < HD, kv_k = t < half;
+    const int tq = min(t, G * half - 1), iq = tq % half, hq = tq / half;
+    const int nq = (g * G + hq) * HD + 2 * iq;
+    const int tk = min(t, HD - 1), ik = tk % half;
+    const int nkv = has_kv ? (kv_k ? qdim + g * HD + 2 * tk : qdim + kvdim + g * HD + 2 * (tk - half)) : nq;
+    // all partials requested together (decode_attention_fuses_qkv: at most
+    // DEC_QKV_SPLITS splits)
+    constexpr int U = DEC_QKV_SPLITS;
+    const float csq = qp.rope_cos[(int64_t)pos * half + iq], snq = qp.rope_sin[(int64_t)pos * half + iq];
+    const float csk = qp.rope_cos[(int64_t)pos * half + ik], snk = qp.rope_sin[(int64_t)pos * half + ik];
+    const int64_t kvo = kv_block_base(kv, layer, slot, pos, g);
+    float2 pq[U], pk[U];
+    float q0 = 0.f, q1 = 0.f, k0 = 0.f, k1 = 0.f;
+#define DA_PARTS(s0)                                                                            \
+  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                               \
+    const int64_t r = (int64_t)min((s0) + u, qp.splits - 1) * M + m;                            \
+    pq[u] = *(const float2 *)(qp.part + r * qp.N + nq);                                         \
+    pk[u] = *(const float2 *)(qp.part + r * qp.N + nkv);                                        \
+  }
+// splits past the count add +0, which leaves every sum as it is (a sum that
+// starts at +0 is never -0), and keeps each load's use unconditional
+#define DA_SUM(s0)                                                                              \
+  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                               \
+    /* the partials are in registers here: no load is deferred into a branch */                 \
+    asm volatile("" ::"v"(pq[u].x), "v"(pq[u].y), "v"(pk[u].x), "v"(pk[u].y));                  \
+  }                                                                                             \
+  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                               \
+    const bool in_ = (s0) + u < qp.splits;                                                      \
+    q0 += in_ ? pq[u].x : 0.f;                                                                  \
+    q1 += in_ ? pq[u].y : 0.f;                                                                  \
+    k0 += in_ ? pk[u].x : 0.f;                                                                  \
+    k1 += in_ ? pk[u].y : 0.f;                                                                  \
+  }
+    DA_PARTS(0)
+    DA_SUM(0)
+    {
+      // this wave's K fragments: their block id arrived with the partials
+      // (requested before them); unconditional (a wave without a block
+      // reads the cache's first block, zeroed below)
+      const T *kb = (const T *)kv.k + base;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
+        for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
+    }
+#undef DA_PARTS
+#undef DA_SUM
+    if (nvalid <= 0) {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = zero8<T>();
+    }
+    if (has_q) {
+      float r0, r1;
+      rope_rotate(q0, q1, csq, snq, r0, r1);
+      qls[hq][iq] = Act<T>::st(r0);
+      qls[hq][iq + half] = Act<T>::st(r1);
+    }
+    if (has_kv) {
+      T *kc = (T *)kv.k + kvo + (int64_t)(pos % KV_BLOCK) * HD;
+      T *vc = (T *)kv.v + kvo + pos % KV_BLOCK;
+      if (kv_k) {
+        float r0, r1;
+        rope_rotate(k0, k1, csk, snk, r0, r1);
+        const T t0 = Act<T>::st(r0), t1 = Act<T>::st(r1);
+        kvn[0][ik] = t0;
+        kvn[0][ik + half] = t1;
+        kc[ik] = t0;
+        kc[ik + half] = t1;
+      } else {
+        const int j = 2 * (tk - half);
+        const T t0 = Act<T>::st(k0), t1 = Act<T>::st(k1);
+        kvn[1][j] = t0;
+        kvn[1][j + 1] = t1;
+        vc[(int64_t)j * KV_BLOCK] = t0;
+        vc[(int64_t)(j + 1) * KV_BLOCK] = t1;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qa[ks] = (r16 < G) ? load8<T>(&qls[r16][ks * 32 + kq]) : zero8<T>();
+    if (pnew >= 0 && pnew < 64) {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+        if (nt * 16 + r16 == pnew) {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(&kvn[0][ks * 32 + kq]);
+        }
+    }
   } else {
+    const T *qrow = q + ((int64_t)m * n_heads + g * G + (r16 < G ? r16 : 0)) * HD;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int ks = 0; ks < KS; ++ks) qa[ks] = (r16 < G) ? load8<T>(qrow + ks * 32 + kq) : zero8<T>();
+    if (nvalid > 0) {
+      const T *kb = (const T *)kv.k + base;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = zero8<T>();
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
+    } else {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = zero8<T>();
+    }
   }
   floatx4_t sacc[4];
 #pragma unroll
@@ -324,6 +449,19 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (kk * 32 + kq + e >= nvalid) vf[nt][kk][e] = (typename Mfma<T>::v8){}[0];
+  }
+  // the row's new V entry (FUSED), in place of what the cache held there
+  if (FUSED && pnew >= 0 && pnew < 64) {
+    typedef __typeof__((typename Mfma<T>::v8){}[0]) elem_t;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const elem_t vn = __builtin_bit_cast(elem_t, kvn[FUSED ? 1 : 0][nt * 16 + r16]);
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kk * 32 + kq + e == pnew) vf[nt][kk][e] = vn;
+    }
   }
   // sacc[nt][i]: row (head) 4*quad + i, position nt*16 + r16
   const float scale = rsqrtf((float)HD);
@@ -397,25 +535,36 @@ __global__ __launch_bounds__(256) void decode_attn_mfma_kernel(const T *__restri
 
 template <typename T, int HD, int G>
 static void launch_decode_group(dim3 grid, const T *q, const RowMeta &rows, const KVCache &kv, int layer, int M,
-                                int n_heads, int max_ctx, int splits, float *ws, hipStream_t s) {
-  if constexpr (sizeof(T) == 2)
-    decode_attn_mfma_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits, ws);
-  else
+                                int n_heads, int max_ctx, int splits, float *ws, hipStream_t s, const QkvParts *qkv) {
+  if constexpr (sizeof(T) == 2) {
+    if constexpr (G * HD / 2 <= 256) {
+      if (qkv) {
+        decode_attn_mfma_kernel<T, HD, G, true><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits,
+                                                                     ws, *qkv);
+        return;
+      }
+    }
+    decode_attn_mfma_kernel<T, HD, G, false><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits,
+                                                                    ws, QkvParts{});
+  } else {
     decode_attn_kernel<T, HD, G><<<grid, 256, 0, s>>>(q, rows, kv, layer, M, n_heads, max_ctx, splits, ws);
+  }
 }
 
 template <typename T, int HD>
 static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s) {
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s,
+                             const QkvParts *qkv) {
   const int G = n_heads / kv.n_kv_heads;
+  if (qkv && !decode_attention_fuses_qkv(G, HD, qkv->splits)) return;
   const int splits = (max_ctx + DEC_CHUNK - 1) / DEC_CHUNK;
   if (items <= 0 || items > M * splits) items = M * splits;
   dim3 grid((unsigned)(items * kv.n_kv_heads));
   switch (G) {
-    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
-    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
-    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
-    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s); break;
+    case 1: launch_decode_group<T, HD, 1>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s, qkv); break;
+    case 2: launch_decode_group<T, HD, 2>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s, qkv); break;
+    case 4: launch_decode_group<T, HD, 4>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s, qkv); break;
+    case 8: launch_decode_group<T, HD, 8>(grid, q, rows, kv, layer, M, n_heads, max_ctx, splits, ws, s, qkv); break;
     default: return;
   }
   decode_combine_kernel<T, HD><<<dim3(n_heads, M), HD, 0, s>>>(rows, n_heads, max_ctx, splits, ws, out);
@@ -423,12 +572,14 @@ static void launch_decode_hd(const T *q, T *out, const RowMeta &rows, const KVCa
 
 template <typename T>
 void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s) {
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s,
+                             const QkvParts *qkv) {
   if (M <= 0) return;
+  if (sizeof(T) != 2) qkv = nullptr;  // the fp32 path has no split QKV projection
   if (kv.head_dim == 128)
-    launch_decode_hd<T, 128>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s);
+    launch_decode_hd<T, 128>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s, qkv);
   else if (kv.head_dim == 64)
-    launch_decode_hd<T, 64>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s);
+    launch_decode_hd<T, 64>(q, out, rows, kv, layer, M, n_heads, max_ctx, items, ws, s, qkv);
 }
 
 // ------------------------------------------------------------------ prefill
@@ -679,7 +830,8 @@ void launch_prefill_attention(const T *q, T *out, const int32_t *seq_start, cons
 
 #define INST(T)                                                                                     \
   template void launch_decode_attention<T>(const T *, T *, const RowMeta &, const KVCache &, int,   \
-                                           int, int, int, int, float *, hipStream_t);               \
+                                           int, int, int, int, float *, hipStream_t,                \
+                                           const QkvParts *);                                       \
   template void launch_prefill_attention<T>(const T *, T *, const int32_t *, const int32_t *, int, \
                                             int, const KVCache &, int, int, hipStream_t);
 INST(float)

@@ -733,12 +733,19 @@ int run_layers(lp_engine *e, bool prefill, int M, int n_out, int n_seq, int max_
     eq.rope_cos = e->ptr<float>(e->Ly.rope_cos);
     eq.rope_sin = e->ptr<float>(e->Ly.rope_sin);
     launch_gemm<T>(xn, D.d, e->ptr<T>(e->Ly.wqkv[l]), M, D.qkv_n, D.d, s_qkv, part, eq, st);
-    if (s_qkv > 1) launch_gemm_finish<T>(part, s_qkv, M, D.qkv_n, eq, st);
-    if (prefill)
+    // a decode step's split QKV projection is finished inside the attention
+    // kernel (sum of partials, rotary embedding, KV append); prefill finishes
+    // it in its own pass
+    const bool fuse_qkv = !prefill && bf && s_qkv > 1 && !(e->opt.flags & LP_FLAG_SEPARATE_QKV_FINISH) &&
+                          decode_attention_fuses_qkv(D.Hq / D.Hkv, D.hd, s_qkv);
+    if (s_qkv > 1 && !fuse_qkv) launch_gemm_finish<T>(part, s_qkv, M, D.qkv_n, eq, st);
+    if (prefill) {
       launch_prefill_attention<T>(qb, ab, dm.seq_start, dm.seq_slot, n_seq, max_len, kv, l, D.Hq, st);
-    else
+    } else {
+      const QkvParts qp{part, s_qkv, D.qkv_n, eq.rope_cos, eq.rope_sin};
       launch_decode_attention<T>(qb, ab, rows, kv, l, M, D.Hq, max_len, attn_items, e->ptr<float>(e->Ly.attn_ws),
-                                 st);
+                                 st, fuse_qkv ? &qp : nullptr);
+    }
     Epi eo{};
     eo.kind = EPI_RESID;
     eo.out = x;

@@ -123,11 +123,27 @@ void launch_gemm_finish(const float *part, int splits, int M, int N, const Epi &
 // rows' total chunk count, the sum of decode_attention_chunks(ctx) over the
 // rows, which sizes the grid to the live work; 0 launches the upper bound
 // M * decode_attention_chunks(max_ctx), whose surplus workgroups exit.
+//
+// With `qkv` (16-bit types only): q is not read.  The attention kernel
+// finishes the split-K QKV projection itself: it sums the fp32 partials
+// [splits][M][N] of its row and heads in split order, applies the rotary
+// embedding to q and k, writes the row's new K and V entry into the cache
+// (the workgroup of the row's last chunk) and uses that entry in registers,
+// all with the arithmetic of launch_gemm_finish's EPI_QKV epilogue.
+struct QkvParts {
+  const float *part;  // [splits][M][N] fp32, N = (Hq + 2 Hkv) hd, rotary pairs adjacent
+  int splits, N;
+  const float *rope_cos, *rope_sin;  // [positions][hd / 2]
+};
+// Whether launch_decode_attention can take `qkv` for a query-head group of
+// that size and that many QKV splits (it launches nothing where it cannot).
+bool decode_attention_fuses_qkv(int group, int head_dim, int splits);
 size_t decode_attention_ws_bytes(int M, int n_heads, int head_dim, int max_ctx);
 int decode_attention_chunks(int ctx);
 template <typename T>
 void launch_decode_attention(const T *q, T *out, const RowMeta &rows, const KVCache &kv, int layer,
-                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s);
+                             int M, int n_heads, int max_ctx, int items, float *ws, hipStream_t s,
+                             const QkvParts *qkv = nullptr);
 
 // Prefill (causal) attention over packed sequences: sequence j covers rows
 // [seq_start[j], seq_start[j+1]) at positions 0.., KV slot seq_slot[j].

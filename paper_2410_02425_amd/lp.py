@@ -16,7 +16,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 LP_OK, LP_EINVAL, LP_ENOMEM, LP_EHIP, LP_ESTATE = 0, -1, -2, -3, -4
 LP_F32, LP_BF16, LP_F16 = 0, 1, 2
 LP_OPEN_LOOP, LP_CLOSED_LOOP = 0, 1
-LP_FLAG_KEEP_LOGITS, LP_FLAG_TIME_KERNEL, LP_FLAG_BF16_ACTIVATIONS = 1, 2, 4
+LP_FLAG_KEEP_LOGITS, LP_FLAG_TIME_KERNEL, LP_FLAG_BF16_ACTIVATIONS, LP_FLAG_SEPARATE_QKV_FINISH = 1, 2, 4, 8
 
 EXPORTED = [
     "lp_arena_bytes_required", "lp_engine_create", "lp_load_weights", "lp_init_weights_random",

@@ -391,6 +391,37 @@ def test_8b_two_layers_large_prefill_two_workgroups_per_cu():
     assert rows == 64 and full_width_check.max_prefill_tokens == M  # all 64 prompts in one prefill step
 
 
+def test_decode_qkv_finish_fused_matches_separate_pass():
+    """Decode steps finish the split QKV projection inside the attention
+    kernel; LP_FLAG_SEPARATE_QKV_FINISH runs the separate finishing pass
+    instead.  Same logits bit for bit over a teacher-forced 8B-shape run (two
+    layers, 64 slots, 5-way split QKV at 64 rows), with new positions on
+    64-position block and 256-position chunk boundaries (63, 64, 255, 256,
+    511, 512) so that the new K/V entry lands in every wave of the chunk."""
+    shape = synth.SHAPES["8b"].with_layers(2)
+    rng = np.random.default_rng(77)
+    lens = [61, 62, 63, 64, 126, 127, 128, 253, 254, 255, 256, 257, 300, 509, 510, 511]
+    lens += [int(x) for x in rng.integers(1, 400, size=64 - len(lens))]
+    reqs, forced = [], {}
+    for i, n_in in enumerate(lens):
+        n_out = 4
+        reqs.append(synth.Request(i, rng.integers(0, shape.vocab, size=n_in).astype(np.int32), n_out))
+        forced[i] = rng.integers(0, shape.vocab, size=n_out - 1).tolist()
+    got = []
+    for extra in (0, lp.LP_FLAG_SEPARATE_QKV_FINISH):
+        eng = engine_for(shape, 64, 520, flags=lp.LP_FLAG_KEEP_LOGITS | extra, max_prefill=32768)
+        eng.init_weights_random(0x5EED, 0.02)
+        eng.submit(reqs)
+        for r in reqs:
+            eng.set_forced_tokens(r.id, forced[r.id])
+        eng.run(lp.LP_CLOSED_LOOP, 64)
+        assert max(s["n_rows"] for s in eng.step_log() if s["kind"] == "decode") == 64
+        got.append({r.id: np.stack([eng.logits(r.id, k) for k in range(r.out_len)]) for r in reqs})
+        eng.close()
+    for r in reqs:
+        assert np.array_equal(got[0][r.id], got[1][r.id]), r.id
+
+
 @pytest.mark.parametrize("name,layers,lens,act", FULL_WIDTH_CASES)
 def test_full_width_teacher_forced(name, layers, lens, act):
     """A configuration's shape at full width and reduced depth."""
