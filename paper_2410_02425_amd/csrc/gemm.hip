@@ -681,10 +681,13 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
 //     one tile's time at the tile shape's measured per-CU rate (4.8 TFLOP/s
 //     for 256-row tiles, 4.5 for the software-pipelined 128-row ones, which
 //     waste fewer padded rows at small M and give more tiles), plus the fp32
-//     partials of a split written and read once at 5 TB/s.  Splits keep at
-//     least 1024 K each.  Fitted to a sweep of the decoder's four projections
-//     over M = 300..4096, it picks within 3% of the measured best in 23 of 24
-//     cases.
+//     partials of a split written and read once at 5 TB/s.  Splits of 1 to
+//     8, keeping at least 1024 K each.  Fitted to a sweep of the decoder's
+//     four projections over M = 300..4096 at splits 1, 2 and 4, it picked
+//     within 3% of the measured best in 23 of 24 cases; the split counts in
+//     between (3, 5, 6) fill the 256 CUs better at prompt sizes of a few
+//     hundred tokens (8B down at M = 632 with its partials' fold: 124 us at
+//     2 splits, 96 at 3).
 //   * Two 128-row workgroups per CU (only with at least 512 tiles and no
 //     split: with fewer, the dispatcher pairs workgroups on some CUs while
 //     others idle): full rounds of 512 tiles at 4.86 TFLOP/s per CU, then a
@@ -738,7 +741,7 @@ static PrefillPlan prefill_plan(int M, int N, int K, int splits) {
   PrefillPlan best{256, 1, false};
   if (M <= 64 || K % PF_KQ != 0) return best;
   double tbest = -1.0;
-  for (int s : {1, 2, 4}) {
+  for (int s = 1; s <= 8; ++s) {
     if (splits > 0 ? s != 1 : (s > 1 && K / s < 1024)) continue;
     const int req = splits > 0 ? splits : s;
     for (int bm : {256, 128}) {

@@ -54,6 +54,9 @@ GEMM_CASES = [
     # plain; 108 tiles of a 283 MB weight, grouped; 65 tiles with 256-row
     # tiles, grouped, and split K, plain)
     (700, 22000, 4096, 1), (600, 27600, 5120, 1), (600, 16500, 1024, 1), (300, 16500, 2048, 2),
+    # odd split counts the planner takes for prompts of a few hundred tokens
+    # (8B O at 553 rows: 3 splits; a 5-way split of a long K with tails)
+    (553, 4096, 4096, 3), (632, 1000, 6400, 5),
 ]
 
 # the kernel each case above is planned to take (the plan is host logic):
