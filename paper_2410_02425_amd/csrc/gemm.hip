@@ -678,21 +678,24 @@ __global__ __launch_bounds__(PF_NT, WPE) void gemm_prefill_kernel(const T *__res
 // Tile rows, K splits and workgroups per CU of a prefill GEMM, chosen by an
 // estimate of its time.
 //   * One workgroup per CU: the rounds of workgroups over the 256 CUs times
-//     one tile's time at the tile shape's measured per-CU rate (4.8 TFLOP/s
-//     for 256-row tiles, 4.5 for the software-pipelined 128-row ones, which
-//     waste fewer padded rows at small M and give more tiles), plus the fp32
-//     partials of a split written and read once at 5 TB/s.  Splits of 1 to
-//     8, keeping at least 1024 K each.  Fitted to a sweep of the decoder's
-//     four projections over M = 300..4096 at splits 1, 2 and 4, it picked
-//     within 3% of the measured best in 23 of 24 cases; the split counts in
-//     between (3, 5, 6) fill the 256 CUs better at prompt sizes of a few
-//     hundred tokens (8B down at M = 632 with its partials' fold: 124 us at
-//     2 splits, 96 at 3).
+//     one tile's time at the tile shape's per-CU rate (PF_RATE_256,
+//     PF_RATE_128), plus the fp32 partials of a split written and read once
+//     (PF_FOLD_RATE, the folding pass included).  Splits of 1 to 8, keeping
+//     at least 1024 K each.
 //   * Two 128-row workgroups per CU (only with at least 512 tiles and no
 //     split: with fewer, the dispatcher pairs workgroups on some CUs while
-//     others idle): full rounds of 512 tiles at 4.86 TFLOP/s per CU, then a
-//     remainder of at most 256 tiles one per CU at the single-tile rate, or a
+//     others idle): full rounds of 512 tiles at PF_RATE_PAIR per CU, then a
+//     remainder of at most 256 tiles one per CU at the 128-row rate, or a
 //     larger one as one more paired round.
+// The rates were fitted to a sweep of every plan (tile rows, 1-8 splits,
+// paired or not), each timed with the pass that consumes its partials, for
+// the projections of the 8B, 13B and 70B shapes at M = 150..38,156: the plan
+// picked is on average 0.15% (8B up to 4,223 rows), 0.6% (13B, 70B) and 0.6%
+// (8B, 3,000 to 38,156 rows) slower than the best measured one, 9% at worst
+// (13B down at M = 1,067), against 1.7%, 2.7% and 2.0% for the earlier rates
+// (4.5, 4.8, 4.86 TFLOP/s, partials at 5 TB/s).
+static constexpr double PF_RATE_128 = 4.1e12, PF_RATE_256 = 5.2e12, PF_RATE_PAIR = 4.86e12;  // flop/s per CU
+static constexpr double PF_FOLD_RATE = 4.0e12;  // bytes/s of split partials, written and read back
 static int prefill_kchunk(int K, int s) { return (K / s + PF_KQ - 1) / PF_KQ * PF_KQ; }
 
 static double prefill_cost(int M, int N, int K, int bm, int s) {
@@ -700,8 +703,8 @@ static double prefill_cost(int M, int N, int K, int bm, int s) {
   const int se = (K + kchunk - 1) / kchunk;
   const int64_t wgs = (int64_t)((M + bm - 1) / bm) * ((N + PF_BN - 1) / PF_BN) * se;
   const double rounds = (double)((wgs + 255) / 256);
-  const double rate = bm == 256 ? 4.8e12 : 4.5e12;
-  const double partials = se > 1 ? 2.0 * se * M * N * 4 / 5e12 : 0.0;
+  const double rate = bm == 256 ? PF_RATE_256 : PF_RATE_128;
+  const double partials = se > 1 ? 2.0 * se * M * N * 4 / PF_FOLD_RATE : 0.0;
   return rounds * (2.0 * bm * PF_BN * kchunk / rate) + partials;
 }
 
@@ -725,8 +728,8 @@ static double prefill_pair_cost(int M, int N, int K) {
   if (tiles < PF_PAIR_MIN_TILES) return -1.0;
   const double flops = 2.0 * 128 * PF_BN * K;
   const int64_t rest = tiles % 512;
-  const double tail = rest == 0 ? 0.0 : (rest <= 256 ? flops / 4.5e12 : 2.0 * flops / 4.86e12);
-  return (double)(tiles / 512) * 2.0 * flops / 4.86e12 + tail;
+  const double tail = rest == 0 ? 0.0 : (rest <= 256 ? flops / PF_RATE_128 : 2.0 * flops / PF_RATE_PAIR);
+  return (double)(tiles / 512) * 2.0 * flops / PF_RATE_PAIR + tail;
 }
 
 struct PrefillPlan {
