@@ -122,17 +122,26 @@ Layout plan_layout(const lp_model_config &c, const lp_engine_options &o, int64_t
     off = align256(off + bytes);
     return at;
   };
-  Ly.embed = take((size_t)D.V * D.d * D.esz);
+  // the norm gains first, then the matrices, each on a 2 MiB boundary (no
+  // padding where the matrices' sizes are multiples of 2 MiB, as at every
+  // 16-bit shape here)
+  auto take_w = [&](size_t bytes) {
+    off = (off + KV_ALIGN - 1) / KV_ALIGN * KV_ALIGN;
+    return take(bytes);
+  };
   for (int l = 0; l < D.L; ++l) {
     Ly.attn_norm.push_back(take((size_t)D.d * 4));
-    Ly.wqkv.push_back(take(wbytes(D, D.qkv_n, D.d)));
-    Ly.wo.push_back(take(wbytes(D, D.d, (int64_t)D.Hq * D.hd)));
     Ly.mlp_norm.push_back(take((size_t)D.d * 4));
-    Ly.wgu.push_back(take(wbytes(D, 2 * (int64_t)D.F, D.d)));
-    Ly.wd.push_back(take(wbytes(D, D.d, D.F)));
   }
   Ly.final_norm = take((size_t)D.d * 4);
-  Ly.lm_head = take(wbytes(D, D.V, D.d));
+  Ly.embed = take_w((size_t)D.V * D.d * D.esz);
+  for (int l = 0; l < D.L; ++l) {
+    Ly.wqkv.push_back(take_w(wbytes(D, D.qkv_n, D.d)));
+    Ly.wo.push_back(take_w(wbytes(D, D.d, (int64_t)D.Hq * D.hd)));
+    Ly.wgu.push_back(take_w(wbytes(D, 2 * (int64_t)D.F, D.d)));
+    Ly.wd.push_back(take_w(wbytes(D, D.d, D.F)));
+  }
+  Ly.lm_head = take_w(wbytes(D, D.V, D.d));
   Ly.weights_end = off;
   // every workspace buffer starts on a 2 MiB boundary as well: its alignment
   // then does not depend on the sizes of the buffers before it

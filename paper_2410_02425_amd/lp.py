@@ -189,6 +189,9 @@ def arena_bytes(cfg: ModelConfig, opt: EngineOptions) -> int:
     return out.value
 
 
+ARENA_ALIGN = 2 << 20
+
+
 class Engine:
     """One serving engine on the current torch device and stream."""
 
@@ -196,9 +199,12 @@ class Engine:
         import torch
         self.cfg, self.opt = cfg, opt
         n = arena_bytes_ if arena_bytes_ is not None else arena_bytes(cfg, opt)
-        self.arena = torch.empty(n, dtype=torch.uint8, device=device)
+        # the engine lays its buffers out on 2 MiB boundaries of the arena:
+        # hand it a 2 MiB-aligned start (the allocation has that much slack)
+        self.arena = torch.empty(n + ARENA_ALIGN, dtype=torch.uint8, device=device)
+        base = (self.arena.data_ptr() + ARENA_ALIGN - 1) // ARENA_ALIGN * ARENA_ALIGN
         h = C.c_void_p()
-        _check(lib().lp_engine_create(C.byref(cfg), C.byref(opt), _ptr(self.arena), n, _stream(), C.byref(h)))
+        _check(lib().lp_engine_create(C.byref(cfg), C.byref(opt), C.c_void_p(base), n, _stream(), C.byref(h)))
         self.h = h
         self._reqs = {}
 
