@@ -77,6 +77,11 @@ __global__ __launch_bounds__(NW * KW * 64) void gemm_skinny_kernel(const T *__re
   const int kbeg = blockIdx.y * kchunk + kw * kcw, kend = min(K, kbeg + kcw);
   const int klen = KW == 1 ? kend - kbeg : kcw;
   const int nsub = ((klen + 2 * KC - 1) / (2 * KC)) * 2;
+  // every workgroup has K to cover, so the loop below runs at least once;
+  // told so, the compiler keeps the first weight and activation requests
+  // ahead of the prologue's barrier instead of sinking them into the loop's
+  // preheader behind the first activation round trip
+  __builtin_assume(nsub >= 2);
 #define SK_SC(c) (kbeg + (c) * KC)
   const int klast = SK_SC(nsub - 1);
 
