@@ -440,29 +440,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FUSED ? 4 :
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) vf[nt][0] = vf[nt][1] = zero8<T>();
   }
-  // positions past the context hold stale or uninitialised cache entries
-  if (nvalid < 64) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (kk * 32 + kq + e >= nvalid) vf[nt][kk][e] = (typename Mfma<T>::v8){}[0];
-  }
-  // the row's new V entry (FUSED), in place of what the cache held there
-  if (FUSED && pnew >= 0 && pnew < 64) {
-    typedef __typeof__((typename Mfma<T>::v8){}[0]) elem_t;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const elem_t vn = __builtin_bit_cast(elem_t, kvn[FUSED ? 1 : 0][nt * 16 + r16]);
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (kk * 32 + kq + e == pnew) vf[nt][kk][e] = vn;
-    }
-  }
   // sacc[nt][i]: row (head) 4*quad + i, position nt*16 + r16
   const float scale = rsqrtf((float)HD);
   float mx[4], sm[4];
@@ -493,6 +470,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FUSED ? 4 :
   v8 pa[2];
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) pa[kk] = load8<T>(&pls[wave][r16][kk * 32 + kq]);
+  // The V fragments are patched only now, after the softmax: a patch waits
+  // for the fragments it edits, and placed right after their loads it held
+  // the softmax of the wave (and, at the barrier above, its workgroup)
+  // behind the V round trip.
+  // Positions past the context hold stale or uninitialised cache entries.
+  if (nvalid < 64) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kk * 32 + kq + e >= nvalid) vf[nt][kk][e] = (typename Mfma<T>::v8){}[0];
+  }
+  // the row's new V entry (FUSED), in place of what the cache held there
+  if (FUSED && pnew >= 0 && pnew < 64) {
+    typedef __typeof__((typename Mfma<T>::v8){}[0]) elem_t;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const elem_t vn = __builtin_bit_cast(elem_t, kvn[FUSED ? 1 : 0][nt * 16 + r16]);
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kk * 32 + kq + e == pnew) vf[nt][kk][e] = vn;
+    }
+  }
   floatx4_t oacc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
