@@ -347,17 +347,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FUSED ? 4 :
     k1 += in_ ? pk[u].y : 0.f;                                                                  \
   }
     DA_PARTS(0)
-    DA_SUM(0)
     {
-      // this wave's K fragments: their block id arrived with the partials
-      // (requested before them); unconditional (a wave without a block
-      // reads the cache's first block, zeroed below)
+      // this wave's K fragments, requested right behind the partials and
+      // before the wait for them, so that the K round trip runs under the
+      // partials' (the wait counter is in order: the partials can be waited
+      // for with these still outstanding); unconditional (a wave without a
+      // block reads the cache's first block, zeroed below)
       const T *kb = (const T *)kv.k + base;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) kf[nt][ks] = load8<T>(kb + (nt * 16 + r16) * HD + ks * 32 + kq);
     }
+    DA_SUM(0)
 #undef DA_PARTS
 #undef DA_SUM
     if (nvalid <= 0) {
