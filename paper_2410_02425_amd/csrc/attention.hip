@@ -667,10 +667,14 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(const T *__restrict__
 // causal mask.  The launch bound (at least two workgroups' worth of waves
 // per SIMD) makes the compiler keep the 128-dim kernel at 148 VGPRs, so three
 // waves share each SIMD and one wave's softmax runs under another's MFMAs.
+// Grid: (query tile, head, sequence), or with longest_first (head, sequence,
+// query tile) with the tiles walked from the last, so that the tiles with the
+// most key blocks are dispatched first and the short ones fill in behind them.
 template <typename T, int HD>
 __global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__restrict__ q, T *__restrict__ out,
                                                                 const int32_t *seq_start, const int32_t *seq_slot,
-                                                                KVCache kv, int layer, int n_heads) {
+                                                                KVCache kv, int layer, int n_heads,
+                                                                int longest_first) {
   typedef typename Mfma<T>::v8 v8;
   constexpr int KS = HD / 32;                 // contraction steps over head_dim
   constexpr int NT = HD / 16;                 // output tiles over head_dim
@@ -680,7 +684,9 @@ __global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__re
   __shared__ T ks[64][KPAD];
   __shared__ T vs[HD][VPAD];
   __shared__ T pls[4][16][64 + 8];
-  const int qt = blockIdx.x, h = blockIdx.y, j = blockIdx.z;
+  const int qt = longest_first ? (int)gridDim.z - 1 - (int)blockIdx.z : (int)blockIdx.x;
+  const int h = longest_first ? (int)blockIdx.x : (int)blockIdx.y;
+  const int j = longest_first ? (int)blockIdx.y : (int)blockIdx.z;
   const int row0 = seq_start[j];
   const int len = seq_start[j + 1] - row0;
   if (qt * 64 >= len) return;
@@ -813,13 +819,25 @@ __global__ __launch_bounds__(256, 2) void prefill_attn_mfma_kernel(const T *__re
   }
 }
 
+// Steps of at most this many prompts dispatch the longest query tiles first:
+// with few prompts the tiles of the most key blocks bound the launch (1.1-1.7x
+// faster for one to three prompts of 547-4,000 tokens).  With many, walking
+// each (prompt, head)'s tiles together keeps its keys and values in the L2
+// (64 prompts of 43k tokens: 0.70 against 0.81 ms the other way).
+constexpr int PF_ATTN_LONGEST_FIRST_MAX_SEQ = 4;
+
 template <typename T, int HD>
 static void launch_prefill_hd(dim3 grid, const T *q, T *out, const int32_t *seq_start, const int32_t *seq_slot,
                               const KVCache &kv, int layer, int n_heads, hipStream_t s) {
-  if constexpr (sizeof(T) == 2)
-    prefill_attn_mfma_kernel<T, HD><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
-  else
+  if constexpr (sizeof(T) == 2) {
+    if ((int)grid.z <= PF_ATTN_LONGEST_FIRST_MAX_SEQ)
+      prefill_attn_mfma_kernel<T, HD><<<dim3(grid.y, grid.z, grid.x), 256, 0, s>>>(q, out, seq_start, seq_slot, kv,
+                                                                                   layer, n_heads, 1);
+    else
+      prefill_attn_mfma_kernel<T, HD><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads, 0);
+  } else {
     prefill_attn_kernel<T, HD><<<grid, 256, 0, s>>>(q, out, seq_start, seq_slot, kv, layer, n_heads);
+  }
 }
 
 template <typename T>
