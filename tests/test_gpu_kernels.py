@@ -394,6 +394,10 @@ PREFILL_CASES = [
     ("bf16", 32, 8, 128, [1, 17, 64, 65, 200]),
     ("f16", 32, 8, 128, [1, 17, 64, 65, 200]),
     ("bf16", 8, 8, 128, [130, 3]),
+    # one to four prompts take the longest-first tile order: one long prompt,
+    # and three of mixed lengths (tiles past a short prompt's end exit)
+    ("f16", 32, 8, 128, [700]),
+    ("bf16", 32, 8, 128, [300, 5, 129]),
     ("bf16", 4, 4, 64, [32, 32, 32, 32]),
     ("f32", 4, 4, 64, [32, 32, 5, 100]),
     ("f32", 8, 2, 64, [70]),
