@@ -129,7 +129,10 @@ int lp_arena_bytes_required(const lp_model_config *cfg, const lp_engine_options 
 
 /* Creates an engine inside `arena` (device memory, 256-byte aligned,
  * `arena_bytes` long) working on `hip_stream` (a hipStream_t, may be NULL for
- * the null stream).  LP_ENOMEM if the arena cannot hold the weights, the
+ * the null stream).  The engine places its weight matrices, workspace buffers
+ * and KV pool on 2 MiB boundaries of the arena's offsets, so an arena that
+ * starts on a 2 MiB boundary puts them on the GPU's large pages (the Python
+ * binding allocates 2 MiB of slack and passes such a start).  LP_ENOMEM if the arena cannot hold the weights, the
  * workspace and a KV cache of max_batch_weight tokens (the paper's OOM while
  * probing the maximum batch weight, Sec. III-C-2). */
 int lp_engine_create(const lp_model_config *cfg, const lp_engine_options *opt, void *arena,
