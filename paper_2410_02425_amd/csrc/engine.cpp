@@ -29,8 +29,8 @@ constexpr int64_t LOGITS_LOG_BYTES = 256ll << 20;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // A large pool sized from the arena holds a multiple of KV_NB_ROUND blocks, so
-// that every layer's part of the K and V pools starts at the same alignment
-// (8B decode step: 5.33 ms at some pool sizes, 5.27 at a multiple of 16).
+// that every layer's part of the K and V pools starts at the same (2 MiB)
+// alignment.
 constexpr int64_t KV_NB_ROUND = 16;
 constexpr size_t KV_ALIGN = 2u << 20;  // offset alignment of the K pool and the workspace buffers in the arena
 
